@@ -1,0 +1,408 @@
+/*
+ * oracle.c - plain, slow CPU oracle of the cache-aware MoE decode step.
+ *
+ * TEST INFRASTRUCTURE.  Only the tests, the smoke check and the benchmark's
+ * CPU-baseline leg load this library; the product path never does.  It shares
+ * no code with the GPU path.
+ *
+ * What it computes, and where the paper defines it:
+ *   - native router p^R = softmax(W^R h), S = TopK(p^R)          (Section 2)
+ *   - Temporal Router p^T = softmax(W^T h), s^T = p^R + p^T      (Section 3.2)
+ *   - post-access retention U_B, the shared cache update        (Algorithm 1)
+ *   - Spatio Router p^S = softmax(W^S h), causal predecessor rho,
+ *     a^T = p^R_{t-1} + p^T_{t-1}, s^ST = a^T + p^S_rho            (Section 3.3)
+ *   - pre-access refinement over Top_R(s^ST)                      (Algorithm 2,
+ *     Section 3.3 last paragraph, Appendix B.2)
+ *   - accounting A, D, P, T and Hit, AdjHit, Load/token           (Section 4.1
+ *     "Metrics")
+ *   - SwiGLU expert FFN on the selected experts ("execute the MoE layer",
+ *     Algorithm 2), in fp64.
+ *
+ * Readings where the paper is silent (each listed in the design notes):
+ *   - Scores use a fixed fp32 arithmetic, "canonical" below, so that a second
+ *     implementation can reproduce every comparison bit for bit: logits are
+ *     summed in fp64 and rounded once to fp32; softmax uses orc_exp (Cody-Waite
+ *     reduction + degree-7 Taylor polynomial), a strided-halving sum and an
+ *     IEEE division; score sums are single fp32 additions.
+ *   - Top-K ranks the fp32 native logits (softmax is monotone); all ties go to
+ *     the lower expert index, argmin ties evict the lower index, replacement
+ *     during refinement needs a strictly higher score.
+ *   - Demand-loaded experts are inserted in ascending index order.
+ *   - Caches start empty; refinement starts at the second token.
+ *   - Gate weights are the selected native probabilities renormalised to 1.
+ *   - Physical residency: per layer the device holds the union of the streams'
+ *     caches in numbered slots; a newly needed expert takes the lowest free
+ *     slot, in ascending expert order.  Refinement and the post-access update
+ *     each end with such a residency event.
+ *
+ * Build: gcc -O2 -ffp-contract=off (no fused multiply-add contraction, no
+ * fast-math); fmaf/rintf/ldexpf are the C library's correctly rounded ones.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_NMAX 1024
+
+/* ------------------------------------------------------------------ */
+/* Canonical fp32 exponential for x <= 0.                              */
+/* ------------------------------------------------------------------ */
+/* ln 2 split (Cody & Waite): the high part keeps the top bits of fl32(ln 2)
+ * with the low 8 bits of its 23-bit fraction cleared, so k*LN2_HI is exact
+ * for |k| < 2^8; the low part is fl32(ln 2 - LN2_HI). */
+static float g_ln2_hi, g_ln2_lo, g_inv_ln2, g_coef[8];
+static int g_init = 0;
+
+static void orc_init_constants(void) {
+    if (g_init) return;
+    double ln2 = log(2.0);
+    float f = (float)ln2;
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    u &= ~(uint32_t)0xFF;
+    memcpy(&g_ln2_hi, &u, 4);
+    g_ln2_lo = (float)(ln2 - (double)g_ln2_hi);
+    g_inv_ln2 = (float)(1.0 / ln2);
+    double fact = 1.0;
+    for (int n = 0; n < 8; ++n) {
+        if (n > 0) fact *= (double)n;
+        g_coef[n] = (float)(1.0 / fact); /* Taylor coefficients 1/n! */
+    }
+    g_init = 1;
+}
+
+void orc_exp_constants(float* out /* [11]: ln2_hi, ln2_lo, inv_ln2, c0..c7 */) {
+    orc_init_constants();
+    out[0] = g_ln2_hi;
+    out[1] = g_ln2_lo;
+    out[2] = g_inv_ln2;
+    for (int n = 0; n < 8; ++n) out[3 + n] = g_coef[n];
+}
+
+float orc_exp(float x) {
+    orc_init_constants();
+    if (x < -80.0f) return 0.0f;
+    float k = rintf(x * g_inv_ln2);           /* nearest integer, ties to even */
+    float r = fmaf(-k, g_ln2_hi, x);          /* exact: x - k*ln2_hi */
+    r = fmaf(-k, g_ln2_lo, r);
+    float p = g_coef[7];
+    for (int n = 6; n >= 0; --n) p = fmaf(p, r, g_coef[n]);   /* Horner */
+    return ldexpf(p, (int)k);
+}
+
+/* Canonical softmax: m = max z; u = exp(z - m); sum by strided halving over
+ * the next power of two (padding with +0): v[i] += v[i + w] for w = P/2 .. 1;
+ * p = u / sum. */
+void orc_softmax(const float* z, int n, float* p) {
+    float m = z[0];
+    for (int e = 1; e < n; ++e)
+        if (z[e] > m) m = z[e];
+    int P = 1;
+    while (P < n) P <<= 1;
+    float v[ORC_NMAX];
+    for (int e = 0; e < P; ++e) v[e] = 0.0f;
+    for (int e = 0; e < n; ++e) {
+        float diff = z[e] - m;
+        p[e] = orc_exp(diff);
+        v[e] = p[e];
+    }
+    for (int w = P / 2; w >= 1; w /= 2)
+        for (int i = 0; i < w; ++i) v[i] = v[i] + v[i + w];
+    for (int e = 0; e < n; ++e) p[e] = p[e] / v[0];
+}
+
+/* ------------------------------------------------------------------ */
+/* Ranking                                                             */
+/* ------------------------------------------------------------------ */
+/* The k largest entries of v in descending order; equal values: lower index
+ * first.  (-0 and +0 compare equal, so they tie.) */
+void orc_topk(const float* v, int n, int k, int32_t* out) {
+    uint8_t taken[ORC_NMAX];
+    memset(taken, 0, (size_t)n);
+    for (int r = 0; r < k; ++r) {
+        int best = -1;
+        for (int e = 0; e < n; ++e) {
+            if (taken[e]) continue;
+            if (best < 0 || v[e] > v[best]) best = e;
+        }
+        taken[best] = 1;
+        out[r] = best;
+    }
+}
+
+/* Lowest-scoring member (allowed[u] != 0); ties: lowest index. -1 if none. */
+static int orc_argmin(const float* s, const uint8_t* allowed, int n) {
+    int best = -1;
+    for (int u = 0; u < n; ++u) {
+        if (!allowed[u]) continue;
+        if (best < 0 || s[u] < s[best]) best = u;
+    }
+    return best;
+}
+
+static int orc_count(const uint8_t* c, int n) {
+    int k = 0;
+    for (int e = 0; e < n; ++e) k += c[e] ? 1 : 0;
+    return k;
+}
+
+/* ------------------------------------------------------------------ */
+/* Algorithm 1: shared post-access cache update U_B(C, S, s)           */
+/* ------------------------------------------------------------------ */
+/* C: membership [N] (0/1), updated in place.  S: the K selected experts.
+ * s: retention priority (s^T).  demand (may be NULL): receives S \ C in
+ * ascending order.  Returns |S \ C|. */
+int orc_update_cache(uint8_t* C, int N, int cap, const int32_t* S, int K, const float* s,
+                     int32_t* demand) {
+    uint8_t sel[ORC_NMAX];
+    memset(sel, 0, (size_t)N);
+    for (int k = 0; k < K; ++k) sel[S[k]] = 1;
+    int32_t D[ORC_NMAX];
+    int nD = 0;
+    for (int e = 0; e < N; ++e)
+        if (sel[e] && !C[e]) D[nD++] = e;     /* demand-loaded selected experts */
+    int size = orc_count(C, N);
+    for (int i = 0; i < nD; ++i) {
+        int e = D[i];
+        if (size < cap) {
+            C[e] = 1;
+            ++size;
+        } else {
+            uint8_t victims[ORC_NMAX];        /* residents not selected now */
+            for (int u = 0; u < N; ++u) victims[u] = (uint8_t)(C[u] && !sel[u]);
+            int v = orc_argmin(s, victims, N);
+            C[v] = 0;
+            C[e] = 1;
+        }
+    }
+    if (demand)
+        for (int i = 0; i < nD; ++i) demand[i] = D[i];
+    return nD;
+}
+
+/* ------------------------------------------------------------------ */
+/* Algorithm 2 refinement: examine Top_R(s^ST) in descending order     */
+/* ------------------------------------------------------------------ */
+/* C updated in place; loaded (may be NULL) receives the proactively loaded
+ * experts in the order they were inserted.  Returns their number. */
+int orc_refine(uint8_t* C, int N, int cap, const float* sST, int R, int32_t* loaded) {
+    int32_t A[ORC_NMAX];
+    if (R > N) R = N;
+    orc_topk(sST, N, R, A);
+    int size = orc_count(C, N);
+    int nP = 0;
+    for (int i = 0; i < R; ++i) {
+        int e = A[i];
+        if (C[e]) continue;
+        if (size < cap) {
+            C[e] = 1;
+            ++size;
+            if (loaded) loaded[nP] = e;
+            ++nP;
+        } else {
+            int v = orc_argmin(sST, C, N);
+            if (sST[e] > sST[v]) {
+                C[v] = 0;
+                C[e] = 1;
+                if (loaded) loaded[nP] = e;
+                ++nP;
+            }
+        }
+    }
+    return nP;
+}
+
+/* ------------------------------------------------------------------ */
+/* Router logits and the expert FFN (textbook definitions, fp64)       */
+/* ------------------------------------------------------------------ */
+/* z_e = fl32( sum_i W[e][i] * h[i] + bias[e] ), accumulated in fp64. */
+void orc_logits(const float* W, const float* h, const float* bias, int N, int d, float* z) {
+    for (int e = 0; e < N; ++e) {
+        double acc = 0.0;
+        const float* w = W + (size_t)e * d;
+        for (int i = 0; i < d; ++i) acc += (double)w[i] * (double)h[i];
+        if (bias) acc += (double)bias[e];
+        z[e] = (float)acc;
+    }
+}
+
+/* y = sum_k g_k * W_down,k ( silu(W_gate,k x) * (W_up,k x) ), fp64.
+ * Wg, Wu: [K][F][d]; Wd: [K][d][F]; silu(a) = a / (1 + exp(-a)). */
+void orc_moe_ffn(const float* Wg, const float* Wu, const float* Wd, const double* g, int K, const float* x,
+                 int d, int F, double* y) {
+    double* act = (double*)malloc(sizeof(double) * (size_t)F);
+    for (int j = 0; j < d; ++j) y[j] = 0.0;
+    for (int k = 0; k < K; ++k) {
+        const float* wg = Wg + (size_t)k * F * d;
+        const float* wu = Wu + (size_t)k * F * d;
+        const float* wd = Wd + (size_t)k * d * F;
+        for (int f = 0; f < F; ++f) {
+            double a = 0.0, b = 0.0;
+            for (int i = 0; i < d; ++i) {
+                a += (double)wg[(size_t)f * d + i] * (double)x[i];
+                b += (double)wu[(size_t)f * d + i] * (double)x[i];
+            }
+            act[f] = a / (1.0 + exp(-a)) * b;
+        }
+        for (int j = 0; j < d; ++j) {
+            double acc = 0.0;
+            for (int f = 0; f < F; ++f) acc += (double)wd[(size_t)j * F + f] * act[f];
+            y[j] += g[k] * acc;
+        }
+    }
+    free(act);
+}
+
+/* Hit = 1 - D/A, AdjHit = (A - D)/(A + P), Load/token = (D + P) S_exp / T in
+ * decimal MB (Section 4.1 "Metrics"). */
+void orc_metrics(int64_t A, int64_t D, int64_t P, int64_t T, double expert_bytes, double* out3) {
+    out3[0] = 1.0 - (double)D / (double)A;
+    out3[1] = (double)(A - D) / (double)(A + P);
+    out3[2] = (double)(D + P) * expert_bytes / 1e6 / (double)T;
+}
+
+/* ------------------------------------------------------------------ */
+/* One decode token for all streams                                    */
+/* ------------------------------------------------------------------ */
+typedef struct {
+    int32_t L, N, K, C, R, S, mode, warmup_tokens;
+} orc_cfg;
+
+enum { ORC_CTR_A = 0, ORC_CTR_HITS, ORC_CTR_D, ORC_CTR_P, ORC_CTR_T, ORC_NCTR };
+
+typedef struct {
+    uint8_t* cache;   /* [S][L][N] logical cache membership                    */
+    float* aT;        /* [S][L][N] s^T of the previous token (full mode)       */
+    float* pS;        /* [S][N]    latest Spatio Router distribution           */
+    int64_t* ctr;     /* [S][L][5] A, hits, D, P, T (counted tokens only)       */
+    int32_t* slot_of; /* [L][N]    physical slot of each expert, -1 = absent   */
+    int64_t* phys;    /* [L][2]    physical fills: demand, proactive (counted)  */
+    int32_t n_slots;  /* physical slots per layer                              */
+    int32_t t;        /* index of the next token                               */
+} orc_state;
+
+typedef struct {      /* optional per-token outputs (any pointer may be NULL) */
+    int32_t* sel;     /* [S][L][K] selected experts, descending native logit   */
+    double* gate;     /* [S][L][K] renormalised selected probabilities         */
+    float* pR;        /* [S][L][N] */
+    float* sT;        /* [S][L][N] */
+    float* sST;       /* [S][L][N] (full mode, t >= 1)                          */
+    int32_t* hits;    /* [S][L] */
+    int32_t* nD;      /* [S][L] */
+    int32_t* nP;      /* [S][L] */
+    int32_t* fills;   /* [L][2] physical fills of this token: demand, proactive */
+} orc_out;
+
+/* Residency event: the layer must now hold the union of the streams' caches.
+ * Experts that left the union free their slots; each newly needed expert, in
+ * ascending order, takes the lowest free slot.  Returns the number of fills. */
+static int orc_residency(const orc_cfg* c, orc_state* st, int l) {
+    const int N = c->N;
+    uint8_t need[ORC_NMAX];
+    memset(need, 0, (size_t)N);
+    for (int s = 0; s < c->S; ++s) {
+        const uint8_t* cs = st->cache + ((size_t)s * c->L + l) * N;
+        for (int e = 0; e < N; ++e)
+            if (cs[e]) need[e] = 1;
+    }
+    int32_t* slot = st->slot_of + (size_t)l * N;
+    for (int e = 0; e < N; ++e)
+        if (slot[e] >= 0 && !need[e]) slot[e] = -1;
+    int fills = 0;
+    for (int e = 0; e < N; ++e) {
+        if (!need[e] || slot[e] >= 0) continue;
+        int chosen = -1;
+        for (int q = 0; q < st->n_slots && chosen < 0; ++q) {
+            int used = 0;
+            for (int u = 0; u < N; ++u)
+                if (slot[u] == q) used = 1;
+            if (!used) chosen = q;
+        }
+        if (chosen < 0) return -1; /* cannot happen: union <= n_slots */
+        slot[e] = chosen;
+        ++fills;
+    }
+    return fills;
+}
+
+/* zR, zT, zS: [S][L][N] fp32 logits of this token (zR already includes any
+ * bias; zS ignored in update-only mode).  Returns 0, or -1 on a broken
+ * invariant. */
+int orc_step(const orc_cfg* c, orc_state* st, const float* zR, const float* zT, const float* zS,
+             orc_out* out) {
+    const int L = c->L, N = c->N, K = c->K, S = c->S;
+    const int full = c->mode == 1;
+    const int t = st->t;
+    const int counted = t >= c->warmup_tokens;
+    float pR[ORC_NMAX], pT[ORC_NMAX], pSn[ORC_NMAX], sT[ORC_NMAX], sST[ORC_NMAX];
+    int32_t sel[ORC_NMAX];
+    for (int l = 0; l < L; ++l) {
+        /* Pre-access refinement (Algorithm 2): needs the previous token's
+         * same-layer scores, so it starts at t = 1. */
+        if (full && t >= 1 && c->R > 0) {
+            for (int s = 0; s < S; ++s) {
+                const size_t sl = (size_t)s * L + l;
+                const float* aT = st->aT + sl * N;       /* p^R_{t-1,l} + p^T_{t-1,l} */
+                const float* pred = st->pS + (size_t)s * N; /* p^S at rho(t,l) */
+                for (int e = 0; e < N; ++e) sST[e] = aT[e] + pred[e];
+                int nP = orc_refine(st->cache + sl * N, N, c->C, sST, c->R, NULL);
+                if (counted) st->ctr[sl * ORC_NCTR + ORC_CTR_P] += nP;
+                if (out && out->nP) out->nP[sl] = nP;
+                if (out && out->sST) memcpy(out->sST + sl * N, sST, sizeof(float) * (size_t)N);
+            }
+            int f = orc_residency(c, st, l);
+            if (f < 0) return -1;
+            if (counted) st->phys[(size_t)l * 2 + 1] += f;
+            if (out && out->fills) out->fills[l * 2 + 1] = f;
+        } else {
+            for (int s = 0; s < S; ++s) {
+                if (out && out->nP) out->nP[(size_t)s * L + l] = 0;
+            }
+            if (out && out->fills) out->fills[l * 2 + 1] = 0;
+        }
+        /* Native routing, access, post-access retention (Algorithm 1). */
+        for (int s = 0; s < S; ++s) {
+            const size_t sl = (size_t)s * L + l;
+            orc_softmax(zR + sl * N, N, pR);
+            orc_softmax(zT + sl * N, N, pT);
+            orc_topk(zR + sl * N, N, K, sel);
+            double gsum = 0.0;
+            for (int k = 0; k < K; ++k) gsum += (double)pR[sel[k]];
+            for (int e = 0; e < N; ++e) sT[e] = pR[e] + pT[e];
+            uint8_t* cache = st->cache + sl * N;
+            int hits = 0;
+            for (int k = 0; k < K; ++k) hits += cache[sel[k]] ? 1 : 0;
+            int nD = orc_update_cache(cache, N, c->C, sel, K, sT, NULL);
+            if (hits + nD != K) return -1;
+            if (orc_count(cache, N) > c->C) return -1;
+            if (full) {
+                memcpy(st->aT + sl * N, sT, sizeof(float) * (size_t)N);
+                orc_softmax(zS + sl * N, N, pSn);
+                memcpy(st->pS + (size_t)s * N, pSn, sizeof(float) * (size_t)N);
+            }
+            if (counted) {
+                int64_t* ctr = st->ctr + sl * ORC_NCTR;
+                ctr[ORC_CTR_A] += K;
+                ctr[ORC_CTR_HITS] += hits;
+                ctr[ORC_CTR_D] += nD;
+                ctr[ORC_CTR_T] += 1;
+            }
+            if (out) {
+                if (out->sel) memcpy(out->sel + sl * K, sel, sizeof(int32_t) * (size_t)K);
+                if (out->gate)
+                    for (int k = 0; k < K; ++k) out->gate[sl * K + k] = (double)pR[sel[k]] / gsum;
+                if (out->pR) memcpy(out->pR + sl * N, pR, sizeof(float) * (size_t)N);
+                if (out->sT) memcpy(out->sT + sl * N, sT, sizeof(float) * (size_t)N);
+                if (out->hits) out->hits[sl] = hits;
+                if (out->nD) out->nD[sl] = nD;
+            }
+        }
+        int f = orc_residency(c, st, l);
+        if (f < 0) return -1;
+        if (counted) st->phys[(size_t)l * 2 + 0] += f;
+        if (out && out->fills) out->fills[l * 2 + 0] = f;
+    }
+    st->t = t + 1;
+    return 0;
+}
