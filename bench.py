@@ -1,0 +1,197 @@
+#!/usr/bin/env python3
+"""Throughput of the cache-aware MoE decode step on one MI355X.
+
+One step = one decode token for every stream through all L MoE layers in
+causal order (router GEMV, cache step, residency and fills, expert FFN).  The
+default workload is the Qwen3-30B-A3B-shaped bf16 slice (L=48, N=128, K=8,
+d=2048, SwiGLU 2048->768->2048, C=32, update-only Temporal Router, 64 streams
+x 512 tokens, AR(1) hidden states); all inputs are synthetic, seeded and
+resident in HBM before the timed region.  The metric is token-layer steps per
+second: streams x layers x timed tokens / time.
+
+Prints one JSON line.  Besides the throughput it carries the roofline of the
+dominant kernel (expert gate/up) from HIP events recorded around each of its
+launches during the timed region, the cache statistics (Hit, AdjHit,
+Load/token) and the CPU oracle's throughput on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "cache-aware MoE decode token-layer steps/s per GPU; % HBM roofline; hit rate"
+
+
+def describe(w):
+    mode = "update-only Temporal Router" if w.mode == 0 else f"full Spatio-Temporal, R={w.R}"
+    dt = "bf16" if w.dtype == 1 else "fp32"
+    return (f"{w.name}: L={w.L} N={w.N} K={w.K} d={w.d} SwiGLU {w.d}->{w.F}->{w.d} C={w.C} {mode}, "
+            f"{w.S} streams x {w.T} tokens, {dt}, AR(1) rho={w.rho}"
+            + (f", Zipf({w.zipf}) bias" if w.zipf else ""))
+
+
+def cpu_baseline(w, budget_s):
+    """The oracle on stream 0, tokens 0.. until budget_s of oracle compute."""
+    import numpy as np
+
+    import oracle
+    import synth
+    full = w.mode == 1
+    WR = [synth.router_host(w, synth.KIND_ROUTER_NATIVE, l) for l in range(w.L)]
+    WT = [synth.router_host(w, synth.KIND_ROUTER_TEMPORAL, l) for l in range(w.L)]
+    WS = [synth.router_host(w, synth.KIND_ROUTER_SPATIO, l) for l in range(w.L)] if full else None
+    bias = synth.zipf_bias(w)
+    Tmax = 64
+    H = [synth.hidden_host(w, 0, l, T=Tmax) for l in range(w.L)]
+    experts = {}
+    run = oracle.Run(w.L, w.N, w.K, w.C, w.R, 1, w.mode)
+    busy = 0.0
+    tokens = 0
+    while tokens < Tmax and (tokens == 0 or busy < budget_s):
+        t = tokens
+        t0 = time.perf_counter()
+        z = np.empty((3, 1, w.L, w.N), np.float32)
+        for l in range(w.L):
+            z[0, 0, l] = oracle.logits(WR[l], H[l][t], None if bias is None else bias[l])
+            z[1, 0, l] = oracle.logits(WT[l], H[l][t])
+            if full:
+                z[2, 0, l] = oracle.logits(WS[l], H[l][t])
+        out = run.step(z[0], z[1], z[2] if full else None)
+        busy += time.perf_counter() - t0
+        for l in range(w.L):
+            sel = out["sel"][0, l]
+            for e in sel:  # host input generation is not oracle work: not timed
+                if (l, int(e)) not in experts:
+                    experts[(l, int(e))] = synth.expert_host(w, l, int(e))
+            t0 = time.perf_counter()
+            ex = [experts[(l, int(e))] for e in sel]
+            oracle.moe_ffn(np.stack([a for a, _, _ in ex]), np.stack([b for _, b, _ in ex]),
+                           np.stack([c for _, _, c in ex]), out["gate"][0, l], H[l][t])
+            busy += time.perf_counter() - t0
+        tokens += 1
+    return {"value": tokens * w.L / busy, "unit": "token-layer steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"stream 0, tokens 0..{tokens - 1}, all {w.L} layers (router logits, cache step, "
+                      f"SwiGLU FFN of the {w.K} selected experts), single thread, {busy:.1f} s of oracle time"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed decode tokens (default: T - warmup)")
+    ap.add_argument("--warmup", type=int, default=16, help="untimed decode tokens before the timed region")
+    ap.add_argument("--workload", default="qwen3_30b")
+    ap.add_argument("--C", type=int, default=None)
+    ap.add_argument("--R", type=int, default=None)
+    ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
+    ap.add_argument("--no-profile", action="store_true", help="no per-kernel HIP events in the timed region")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the path shards by stream "
+              "with no exchange, so the multi-GPU figure is not measured here", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2609_04895_amd import cmoe as B
+    from paper_2609_04895_amd.workload import engine_for
+
+    w = synth.WORKLOADS[args.workload]
+    if args.C is not None or args.R is not None:
+        w = w.replace(C=w.C if args.C is None else args.C, R=w.R if args.R is None else args.R)
+    warmup = args.warmup
+    steps = args.steps if args.steps is not None else max(1, w.T - warmup)
+    T_gen = min(w.T, warmup + steps)
+    print(f"[bench] {describe(w)}; warmup {warmup}, timed {steps}", file=sys.stderr, flush=True)
+
+    t0 = time.time()
+    inputs = synth.device_inputs(w, T=T_gen)
+    print(f"[bench] inputs generated on the device in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    eng = engine_for(w, inputs, warmup_tokens=warmup, side_stream=not args.fill_on_main)
+    hidden = inputs["hidden"]
+    y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
+    main_stream = eng.main_stream
+
+    for t in range(warmup):
+        eng.cmoe_step(hidden[t % T_gen], y)
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+
+    if not args.no_profile:
+        eng.cmoe_profile_begin(steps, kernels=("ffn_up",))
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(main_stream)
+    for t in range(warmup, warmup + steps):
+        eng.cmoe_step(hidden[t % T_gen], y)
+    ev1.record(main_stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    elapsed = ev0.elapsed_time(ev1) / 1e3
+    prof = eng.cmoe_profile_end() if not args.no_profile else None
+    tot, _, _ = eng.cmoe_stats()
+    active = eng.cmoe_read(B.CMOE_VIEW_ACTIVE)
+    print(f"[bench] timed region {elapsed * 1e3:.1f} ms (wall {wall * 1e3:.1f} ms)", file=sys.stderr, flush=True)
+
+    e = w.elem_bytes
+    n_act = int(active.sum())                 # expert weight reads by the FFN over the timed region
+    launches = w.L * steps
+    value = w.S * w.L * steps / elapsed
+    res = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "token-layer steps/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": elapsed / steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == 1 else "f32",
+        "data": "synthetic",
+        "config": {"workload": describe(w), "streams": w.S, "layers": w.L, "experts": w.N, "top_k": w.K,
+                   "capacity": w.C, "refine_budget": w.R if w.mode == 1 else 0,
+                   "mode": "update-only" if w.mode == 0 else "spatio-temporal", "d": w.d, "F": w.F,
+                   "fills": "main stream" if args.fill_on_main else "side stream"},
+    }
+    # algorithmic bytes of one token step: each distinct selected expert read
+    # once, router weights, hidden states in, layer outputs out, fills (read +
+    # write of each copied expert)
+    step_bytes = (n_act * w.expert_bytes + steps * w.L * (w.n_routers * w.N * w.d * e + w.S * w.d * e
+                                                          + w.S * w.d * 4)
+                  + 2 * tot["phys_bytes"]) / steps
+    res["step_hbm"] = {"algorithmic_bytes": step_bytes, "achieved_GBs": step_bytes / (elapsed / steps) / 1e9,
+                       "frac": step_bytes / (elapsed / steps) / 1e9 / HBM_PEAK_GBS}
+    if prof is not None:
+        ms_up, n_up = prof["ffn_up"]
+        avg_s = ms_up / 1e3 / max(n_up, 1)
+        bytes_up = (n_act * 2 * w.F * w.d * e) / launches + w.S * w.d * e + w.S * w.K * w.F * e
+        gbs = bytes_up / avg_s / 1e9
+        res["roofline"] = {"kernel": "ffn_up_bf16" if w.dtype == 1 else "ffn_up_f32", "bound": "hbm",
+                           "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                           "traffic": None, "avg_launch_us": avg_s * 1e6, "algorithmic_bytes_per_launch": bytes_up}
+
+    A, D, P, Tc = tot["accesses"], tot["demand_misses"], tot["proactive_loads"], tot["tokens"]
+    res["cache"] = {"hit": 1 - D / A, "adj_hit": (A - D) / (A + P), "load_mb_per_token": (D + P) * w.expert_bytes
+                    / 1e6 / Tc, "accesses": A, "demand_misses": D, "proactive_loads": P, "tokens": Tc,
+                    "phys_fills": tot["phys_fills"], "distinct_experts_per_layer_step": n_act / launches}
+    print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
+    eng.cmoe_destroy()
+    del inputs, hidden
+    if args.cpu_seconds > 0:
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

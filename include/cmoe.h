@@ -1,0 +1,222 @@
+/*
+ * cmoe.h - C ABI of the cache-aware MoE decode step on one MI355X (gfx950).
+ *
+ * The library runs, for S independent decode streams and L MoE layers in
+ * causal order, one decode token per call:
+ *   - the native router p^R = softmax(W^R h), S_t = TopK(p^R)            (Section 2)
+ *   - the Temporal Router p^T = softmax(W^T h), s^T = p^R + p^T         (Section 3.2)
+ *   - in full mode the Spatio Router p^S = softmax(W^S h) of the causal
+ *     predecessor and the pre-access refinement over Top_R(a^T + p^S)    (Section 3.3,
+ *                                                                         Algorithm 2)
+ *   - the post-access retention update U_C of each per-(stream, layer)
+ *     cache of capacity C                                                (Algorithm 1)
+ *   - the accounting of accesses A, hits, demand misses D, proactive
+ *     loads P, decode tokens T and expert-weight traffic (D + P) S_exp    (Section 4.1)
+ *   - copies of newly needed experts from a cold pool into HBM slots
+ *     (a side HIP stream), and the SwiGLU expert FFN on the resident
+ *     weights ("execute the MoE layer", Algorithm 2).
+ * Notation follows the paper's problem statement (Section 2): L layers, N
+ * experts per layer, native Top-K, per-layer cache capacity C (the paper's
+ * B, with C >= K), refinement budget R (Appendix B.2, "replace_lowest").
+ *
+ * Conventions for every entry point:
+ *   - returns a cmoe_status; nothing throws, aborts or prints;
+ *   - on failure cmoe_last_error() describes the cause (thread-local string,
+ *     valid until the next call on the same thread);
+ *   - device pointers are HIP device addresses (or host-pinned addresses
+ *     where stated); the caller allocates and owns every buffer and both
+ *     streams, which must outlive the handle; the library calls no hipMalloc;
+ *   - a HIP failure is sticky: the call returns CMOE_ERR_HIP and later calls
+ *     on the handle return CMOE_ERR_STATE until cmoe_reset or cmoe_destroy;
+ *   - a handle is used by one host thread at a time.
+ */
+#ifndef CMOE_H
+#define CMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CMOE_OK = 0,
+    CMOE_ERR_INVALID_ARG = -1, /* a value violates the problem statement       */
+    CMOE_ERR_UNSUPPORTED = -2, /* valid, but outside what the kernels handle   */
+    CMOE_ERR_HIP = -3,         /* the HIP runtime reported an error            */
+    CMOE_ERR_STATE = -4        /* handle unusable after an earlier HIP error   */
+} cmoe_status;
+
+typedef enum {
+    CMOE_MODE_TEMPORAL = 0,        /* update-only Temporal Router (Section 3.2)   */
+    CMOE_MODE_SPATIO_TEMPORAL = 1  /* full mode with refinement (Section 3.3)     */
+} cmoe_mode;
+
+typedef enum {
+    CMOE_F32 = 0,  /* fp32 weights and hidden states                          */
+    CMOE_BF16 = 1  /* bf16 weights and hidden states, fp32 accumulation        */
+} cmoe_dtype;
+
+typedef enum {
+    CMOE_POOL_DEVICE = 0,      /* cold pool in device memory                  */
+    CMOE_POOL_HOST_PINNED = 1  /* cold pool in pinned, device-mapped host RAM  */
+} cmoe_pool_kind;
+
+/* flags */
+#define CMOE_FLAG_FILL_ON_MAIN 0x1u /* run all fills on the main stream          */
+
+/* Problem shape.  Valid values: 1 <= K <= C <= N (Section 2: capacity at least
+ * Top-K); 0 <= R <= N; L, S >= 1; d, F >= 1; warmup_tokens >= 0.  Supported:
+ * N <= 256, d and F multiples of 64.  R is ignored in CMOE_MODE_TEMPORAL. */
+typedef struct {
+    int32_t L, N, K, d, F, C, R, S;
+    int32_t mode;          /* cmoe_mode                                         */
+    int32_t dtype;         /* cmoe_dtype of weights and hidden states           */
+    int32_t pool_kind;     /* cmoe_pool_kind                                    */
+    int32_t warmup_tokens; /* leading tokens whose transfers are not counted
+                              (the paper excludes prefill transfers)            */
+    uint32_t flags;
+} cmoe_config;
+
+/* Weights (device pointers unless stated).  Router matrices are bias-free
+ * d -> N maps per layer, row-major [L][N][d] in the config dtype.  The cold
+ * pool holds every expert, [L][N] x expert_bytes, each expert laid out as
+ * W_gate[F][d], W_up[F][d], W_down[d][F]; expert_bytes = 3 d F sizeof(dtype).
+ * With CMOE_POOL_HOST_PINNED, cold_pool is a pinned host address mapped into
+ * the device (hipHostMalloc). */
+typedef struct {
+    const void* w_router;    /* W^R [L][N][d]                                    */
+    const void* w_temporal;  /* W^T [L][N][d]                                    */
+    const void* w_spatio;    /* W^S [L][N][d]; required in full mode, else NULL  */
+    const float* logit_bias; /* [L][N] fp32 added to native logits, or NULL      */
+    const void* cold_pool;   /* [L][N][expert_bytes]                             */
+} cmoe_weights;
+
+/* Device buffer sizes in bytes; every buffer must be 256-byte aligned. */
+typedef struct {
+    size_t arena_bytes;     /* HBM expert slots: L x min(N, S C) experts         */
+    size_t state_bytes;     /* caches, scores, counters, slot maps               */
+    size_t workspace_bytes; /* per-step scratch and the inspectable outputs      */
+} cmoe_sizes;
+
+typedef struct {
+    void* arena;
+    void* state;
+    void* workspace;
+} cmoe_buffers;
+
+/* Totals over all streams and layers, counted tokens only.  traffic_bytes =
+ * (demand_misses + proactive_loads) x expert_bytes (Section 4.1 "Metrics");
+ * phys_fills counts expert copies into the HBM slots, phys_bytes their bytes. */
+typedef struct {
+    int64_t accesses, hits, demand_misses, proactive_loads, tokens, traffic_bytes;
+    int64_t phys_fills, phys_bytes;
+} cmoe_stats_t;
+
+typedef struct cmoe_handle cmoe_handle;
+
+/* Buffer sizes for a configuration.  Validates it as cmoe_init does.  Pure host
+ * code: needs no GPU. */
+cmoe_status cmoe_query(const cmoe_config* cfg, cmoe_sizes* out);
+
+/* Binds weights and buffers, clears the state (empty caches, zero counters, no
+ * resident experts) on main_stream and returns a handle.  side_stream may be
+ * NULL (then fills run on main_stream).  Streams are hipStream_t values. */
+cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_buffers* buf,
+                      void* main_stream, void* side_stream, cmoe_handle** out);
+
+/* One decode token for all streams, asynchronous on main_stream.
+ * h: [S][L][d] hidden states h_{t,l} in the config dtype (device).
+ * y: [S][L][d] fp32 output of each MoE layer (device), valid once main_stream
+ *    has completed.  The token index t is kept by the handle. */
+cmoe_status cmoe_step(cmoe_handle* hd, const void* h, float* y);
+
+/* The cache path of one token from given fp32 logits, without the router
+ * GEMV and without the FFN: softmax, Top-K, refinement, access, retention,
+ * counters, residency and fills.  zR (native, bias already added), zT, zS:
+ * [S][L][N] fp32 (device); zS is ignored in update-only mode. */
+cmoe_status cmoe_step_logits(cmoe_handle* hd, const float* zR, const float* zT, const float* zS);
+
+/* Synchronizes both streams and reads the counters.  total may be NULL.
+ * per_stream_layer (or NULL): [S][L][5] int64 = A, hits, D, P, T.
+ * per_layer_phys (or NULL): [L][2] int64 = demand fills, proactive fills. */
+cmoe_status cmoe_stats(cmoe_handle* hd, cmoe_stats_t* total, int64_t* per_stream_layer,
+                       int64_t* per_layer_phys);
+
+/* Reads the cache C of (stream, layer): its experts in ascending order into
+ * experts[0..n) (experts must hold C entries).  Synchronizes. */
+cmoe_status cmoe_get_cache(cmoe_handle* hd, int32_t stream, int32_t layer, int32_t* experts,
+                           int32_t* n);
+
+/* Replaces the cache of (stream, layer) with n <= C distinct experts.  Only the
+ * logical cache changes; physical residency follows at that layer's next
+ * residency event.  Synchronizes. */
+cmoe_status cmoe_set_cache(cmoe_handle* hd, int32_t stream, int32_t layer, const int32_t* experts,
+                           int32_t n);
+
+/* Changes the refinement budget R (0 <= R <= N) for the following tokens; an
+ * inference-time knob that needs no retraining (Section 3.3). */
+cmoe_status cmoe_set_R(cmoe_handle* hd, int32_t R);
+
+/* Empty caches, zero counters and scores, no resident experts, t = 0.  Also
+ * clears a sticky HIP error. */
+cmoe_status cmoe_reset(cmoe_handle* hd);
+
+/* Releases the handle (not the caller's buffers).  NULL is accepted. */
+cmoe_status cmoe_destroy(cmoe_handle* hd);
+
+/* Inspectable state (all synchronize).  Layouts:
+ *   CMOE_VIEW_LOGITS    fp32  [L][S][n_r][N] logits used by the last token,
+ *                              n_r = 2 (native, temporal) or 3 (+ spatio)
+ *   CMOE_VIEW_SELECTED  int32 [L][S][K] selected experts, descending logit
+ *   CMOE_VIEW_GATES     fp32  [L][S][K] renormalised selected probabilities
+ *   CMOE_VIEW_CACHE     u64   [S][L][W] cache membership bit masks,
+ *                              W = ceil(N / 64), expert e is bit e % 64 of word e / 64
+ *   CMOE_VIEW_COUNTERS  int64 [S][L][5] A, hits, D, P, T
+ *   CMOE_VIEW_PHYS      int64 [L][2] physical fills: demand, proactive
+ *   CMOE_VIEW_SLOTS     int32 [L][N] HBM slot of each expert, -1 if absent
+ *   CMOE_VIEW_EVENTS    int32 [L][S][4] last token: hits, D, P, 0
+ *   CMOE_VIEW_FILLS     int32 [L][2] last token's physical fills: demand, proactive
+ *   CMOE_VIEW_ACTIVE    int64 [L] distinct experts executed by the FFN, summed
+ *                              over counted tokens (each is one read of its weights) */
+enum {
+    CMOE_VIEW_LOGITS = 0,
+    CMOE_VIEW_SELECTED = 1,
+    CMOE_VIEW_GATES = 2,
+    CMOE_VIEW_CACHE = 3,
+    CMOE_VIEW_COUNTERS = 4,
+    CMOE_VIEW_PHYS = 5,
+    CMOE_VIEW_SLOTS = 6,
+    CMOE_VIEW_EVENTS = 7,
+    CMOE_VIEW_FILLS = 8,
+    CMOE_VIEW_ACTIVE = 9,
+    CMOE_VIEW_COUNT = 10
+};
+
+/* Bytes of a view (0 for an unknown view or a NULL handle). */
+size_t cmoe_view_bytes(const cmoe_handle* hd, int32_t view);
+
+/* Copies a view into host memory of at least cmoe_view_bytes bytes. */
+cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t bytes);
+
+/* Per-kernel timing with HIP events recorded on the stream each kernel runs
+ * on.  cmoe_profile_begin makes the next max_tokens calls of cmoe_step /
+ * cmoe_step_logits record a start/stop event pair around each launch of the
+ * kernels selected by kernel_mask (bit i = kernel id i; 0 selects all);
+ * cmoe_profile_end synchronizes and returns, per kernel id, the summed
+ * milliseconds and the launch count.  Kernel ids: 0 router GEMV, 1 cache
+ * step, 2 residency and expert grouping, 3 expert gate/up, 4 expert down,
+ * 5 combine, 6 fill.  ms_out and launches_out hold CMOE_KERNEL_COUNT entries.
+ * Event pairs add work between launches; time few kernels at once. */
+#define CMOE_KERNEL_COUNT 7
+cmoe_status cmoe_profile_begin(cmoe_handle* hd, int32_t max_tokens, uint32_t kernel_mask);
+cmoe_status cmoe_profile_end(cmoe_handle* hd, double* ms_out, int64_t* launches_out);
+
+const char* cmoe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CMOE_H */

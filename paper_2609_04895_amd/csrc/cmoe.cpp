@@ -1,0 +1,568 @@
+// cmoe.cpp - host side of the C ABI declared in include/cmoe.h: validation,
+// buffer carving, the per-token launch sequence on the main and side streams,
+// counters, inspection and kernel timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/cmoe.h"
+#include "cmoe_internal.h"
+
+using cmoe::Layout;
+using cmoe::StepArgs;
+
+namespace {
+
+thread_local std::string g_err;
+
+cmoe_status fail(cmoe_status st, const std::string& msg) {
+    g_err = msg;
+    return st;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+enum KernelId { KID_ROUTER = 0, KID_CACHE = 1, KID_FINISH = 2, KID_UP = 3, KID_DOWN = 4, KID_COMBINE = 5, KID_FILL = 6 };
+
+struct Derived {
+    int NW, n_r, n_slots, nsplit, rdk, tiles;
+    size_t esz, expert_bytes;
+};
+
+cmoe_status validate(const cmoe_config* c, Derived* dv) {
+    if (!c) return fail(CMOE_ERR_INVALID_ARG, "config is NULL");
+    if (c->L < 1 || c->S < 1 || c->N < 1 || c->K < 1 || c->d < 1 || c->F < 1)
+        return fail(CMOE_ERR_INVALID_ARG, "L, S, N, K, d and F must be >= 1");
+    if (c->K > c->C) return fail(CMOE_ERR_INVALID_ARG, "capacity C must be at least K");
+    if (c->C > c->N) return fail(CMOE_ERR_INVALID_ARG, "capacity C must not exceed N");
+    if (c->mode != CMOE_MODE_TEMPORAL && c->mode != CMOE_MODE_SPATIO_TEMPORAL)
+        return fail(CMOE_ERR_INVALID_ARG, "unknown mode");
+    if (c->R < 0 || c->R > c->N) return fail(CMOE_ERR_INVALID_ARG, "R must be in [0, N]");
+    if (c->dtype != CMOE_F32 && c->dtype != CMOE_BF16) return fail(CMOE_ERR_INVALID_ARG, "unknown dtype");
+    if (c->pool_kind != CMOE_POOL_DEVICE && c->pool_kind != CMOE_POOL_HOST_PINNED)
+        return fail(CMOE_ERR_INVALID_ARG, "unknown pool kind");
+    if (c->warmup_tokens < 0) return fail(CMOE_ERR_INVALID_ARG, "warmup_tokens must be >= 0");
+    if (c->N > cmoe::kMaxN) return fail(CMOE_ERR_UNSUPPORTED, "N > 256 is not supported");
+    if (c->K > 64) return fail(CMOE_ERR_UNSUPPORTED, "K > 64 is not supported");
+    if (c->d % 64 || c->F % 64) return fail(CMOE_ERR_UNSUPPORTED, "d and F must be multiples of 64");
+    if ((int64_t)c->S * c->K >= (int64_t)1 << 23) return fail(CMOE_ERR_UNSUPPORTED, "S*K too large");
+    dv->NW = (c->N + 63) / 64;
+    dv->n_r = c->mode == CMOE_MODE_SPATIO_TEMPORAL ? 3 : 2;
+    dv->n_slots = (int)std::min<int64_t>(c->N, (int64_t)c->S * c->C);
+    dv->esz = c->dtype == CMOE_BF16 ? 2 : 4;
+    dv->expert_bytes = (size_t)3 * c->d * c->F * dv->esz;
+    // router split-K: enough wavefronts to cover the chip, 32-aligned chunks
+    const int64_t tiles = (int64_t)dv->n_r * ((c->N + 15) / 16) * ((c->S + 15) / 16);
+    if (tiles > (1 << 30)) return fail(CMOE_ERR_UNSUPPORTED, "too many router tiles");
+    dv->tiles = (int)tiles;
+    int rdk = 32;
+    for (int cand : {256, 128, 64, 32}) {
+        if (tiles * ((c->d + cand - 1) / cand) >= 1024) {
+            rdk = cand;
+            break;
+        }
+    }
+    dv->rdk = std::min(rdk, c->d);
+    dv->nsplit = (c->d + dv->rdk - 1) / dv->rdk;
+    // the residency kernel stages the caches and selections of all streams in LDS
+    const size_t lds = (size_t)c->S * dv->NW * 24 + (size_t)c->S * c->K * 4 + (size_t)(c->N + dv->n_slots) * 8;
+    if (lds > cmoe::kMaxFinishLds) return fail(CMOE_ERR_UNSUPPORTED, "S * (24 ceil(N/64) + 4 K) too large");
+    return CMOE_OK;
+}
+
+// Offsets of every sub-buffer; used both for sizing and for carving.
+struct Plan {
+    size_t cache, aT, pS, ctr, phys, active_sum, slot_of, slot_exp, tile_count, state_total;
+    size_t zpart, logits, sel, gates, events, step_fills, fill_list, fill_count, sel_mask, bcount, boffset,
+        pairs, active, n_active, act, yp, ws_total;
+    size_t arena;
+};
+
+Plan make_plan(const cmoe_config* c, const Derived& dv) {
+    Plan p{};
+    const size_t S = c->S, L = c->L, N = c->N, K = c->K;
+    size_t o = 0;
+    auto take = [&o](size_t bytes) {
+        const size_t at = o;
+        o += align256(bytes);
+        return at;
+    };
+    p.cache = take(S * L * dv.NW * 8);
+    p.aT = take(S * L * N * 4);
+    p.pS = take(S * N * 4);
+    p.ctr = take(S * L * cmoe::kNctr * 8);
+    p.phys = take(L * 2 * 8);
+    p.active_sum = take(L * 8);
+    p.slot_of = take(L * N * 4);
+    p.slot_exp = take(L * (size_t)dv.n_slots * 4);
+    p.tile_count = take((size_t)dv.tiles * 4);
+    p.state_total = o;
+    o = 0;
+    p.zpart = take((size_t)dv.tiles * dv.nsplit * 256 * 8);
+    p.logits = take(L * S * dv.n_r * N * 4);
+    p.sel = take(L * S * K * 4);
+    p.gates = take(L * S * K * 4);
+    p.events = take(L * S * 4 * 4);
+    p.step_fills = take(L * 2 * 4);
+    p.fill_list = take(L * 2 * N * 2 * 4);
+    p.fill_count = take(L * 2 * 4);
+    p.sel_mask = take(S * dv.NW * 8);
+    p.bcount = take(N * 4);
+    p.boffset = take(N * 4);
+    p.pairs = take(S * K * 4);
+    p.active = take(N * 4);
+    p.n_active = take(4);
+    p.act = take(S * K * (size_t)c->F * dv.esz);
+    p.yp = take(S * K * (size_t)c->d * 4);
+    p.ws_total = o;
+    p.arena = L * (size_t)dv.n_slots * dv.expert_bytes;
+    return p;
+}
+
+}  // namespace
+
+struct cmoe_handle {
+    cmoe_config cfg;
+    Derived dv;
+    Plan plan;
+    Layout lo;
+    hipStream_t main = nullptr, side = nullptr;
+    bool side_is_main = true;
+    std::vector<hipEvent_t> ev_access, ev_demand, ev_pro;
+    hipEvent_t ev_refine0 = nullptr;
+    int32_t t = 0;
+    int32_t R = 0;
+    bool broken = false;
+    // profiling
+    int32_t prof_left = 0;
+    uint32_t prof_mask = 0;
+    std::vector<hipEvent_t> prof_pool;
+    std::vector<std::pair<int, size_t>> prof_rec;  // kernel id, index of start event (stop = +1)
+    size_t prof_next = 0;
+};
+
+namespace {
+
+cmoe_status hip_fail(cmoe_handle* hd, hipError_t e, const char* where) {
+    if (hd) hd->broken = true;
+    return fail(CMOE_ERR_HIP, std::string("HIP error in ") + where + ": " + hipGetErrorString(e));
+}
+
+#define HIPCHK(expr, where)                               \
+    do {                                                  \
+        hipError_t _e = (expr);                           \
+        if (_e != hipSuccess) return hip_fail(hd, _e, where); \
+    } while (0)
+
+cmoe_status usable(cmoe_handle* hd) {
+    if (!hd) return fail(CMOE_ERR_INVALID_ARG, "handle is NULL");
+    if (hd->broken) return fail(CMOE_ERR_STATE, "handle unusable after an earlier HIP error; call cmoe_reset");
+    return CMOE_OK;
+}
+
+// Records the start event of a timed launch (when profiling) and returns its
+// slot, or SIZE_MAX.
+size_t prof_start(cmoe_handle* hd, int kid, hipStream_t st) {
+    if (hd->prof_left <= 0 || !((hd->prof_mask >> kid) & 1u) || hd->prof_next + 2 > hd->prof_pool.size())
+        return SIZE_MAX;
+    const size_t i = hd->prof_next;
+    hd->prof_next += 2;
+    (void)hipEventRecord(hd->prof_pool[i], st);
+    hd->prof_rec.emplace_back(kid, i);
+    return i;
+}
+
+void prof_stop(cmoe_handle* hd, size_t i, hipStream_t st) {
+    if (i != SIZE_MAX) (void)hipEventRecord(hd->prof_pool[i + 1], st);
+}
+
+template <typename F>
+hipError_t timed(cmoe_handle* hd, int kid, hipStream_t st, F&& launch) {
+    const size_t i = prof_start(hd, kid, st);
+    const hipError_t e = launch();
+    prof_stop(hd, i, st);
+    return e;
+}
+
+// One decode token.  h == nullptr selects injected logits (no router, no FFN).
+cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR, const float* zT, const float* zS) {
+    const cmoe_config& c = hd->cfg;
+    const Layout& lo = hd->lo;
+    const bool inject = h == nullptr;
+    const bool full = c.mode == CMOE_MODE_SPATIO_TEMPORAL;
+    const bool refine_on = full && hd->t >= 1 && hd->R > 0;
+    const uint32_t count = hd->t >= c.warmup_tokens ? cmoe::kFlagCount : 0u;
+    hipStream_t M = hd->main, Sd = hd->side;
+
+    if (refine_on) {  // layer 0: refined from the previous token's last-layer prediction
+        StepArgs a{0, 0, hd->R, cmoe::kFlagRefine | count, zR, zT, zS};
+        HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "refine layer 0");
+        HIPCHK(timed(hd, KID_FINISH, M, [&] { return cmoe::launch_finish(lo, a, M); }), "residency");
+        if (hd->side_is_main) {
+            HIPCHK(timed(hd, KID_FILL, M, [&] { return cmoe::launch_fill(lo, 0, 1, M); }), "fill");
+        } else {
+            HIPCHK(hipEventRecord(hd->ev_refine0, M), "event record");
+            HIPCHK(hipStreamWaitEvent(Sd, hd->ev_refine0, 0), "stream wait");
+            HIPCHK(timed(hd, KID_FILL, Sd, [&] { return cmoe::launch_fill(lo, 0, 1, Sd); }), "fill");
+            HIPCHK(hipEventRecord(hd->ev_pro[0], Sd), "event record");
+        }
+    }
+    for (int l = 0; l < c.L; ++l) {
+        if (!inject) HIPCHK(timed(hd, KID_ROUTER, M, [&] { return cmoe::launch_router(lo, l, h, M); }), "router");
+        if (refine_on && !hd->side_is_main) HIPCHK(hipStreamWaitEvent(M, hd->ev_pro[l], 0), "stream wait");
+        const bool refine_next = refine_on && l + 1 < c.L;
+        uint32_t flags = cmoe::kFlagAccess | count;
+        if (inject) flags |= cmoe::kFlagInject;
+        if (refine_on) flags |= cmoe::kFlagRefinedHere;
+        if (refine_next) flags |= cmoe::kFlagRefine;
+        StepArgs a{l, l + 1, hd->R, flags, zR, zT, zS};
+        HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "cache step");
+        HIPCHK(timed(hd, KID_FINISH, M, [&] { return cmoe::launch_finish(lo, a, M); }), "residency");
+        if (hd->side_is_main) {
+            HIPCHK(timed(hd, KID_FILL, M, [&] { return cmoe::launch_fill(lo, l, 0, M); }), "fill");
+            if (refine_next) HIPCHK(timed(hd, KID_FILL, M, [&] { return cmoe::launch_fill(lo, l + 1, 1, M); }), "fill");
+        } else {
+            HIPCHK(hipEventRecord(hd->ev_access[l], M), "event record");
+            HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[l], 0), "stream wait");
+            HIPCHK(timed(hd, KID_FILL, Sd, [&] { return cmoe::launch_fill(lo, l, 0, Sd); }), "fill");
+            HIPCHK(hipEventRecord(hd->ev_demand[l], Sd), "event record");
+            if (refine_next) {
+                HIPCHK(timed(hd, KID_FILL, Sd, [&] { return cmoe::launch_fill(lo, l + 1, 1, Sd); }), "fill");
+                HIPCHK(hipEventRecord(hd->ev_pro[l + 1], Sd), "event record");
+            }
+            HIPCHK(hipStreamWaitEvent(M, hd->ev_demand[l], 0), "stream wait");
+        }
+        if (!inject) {
+            HIPCHK(timed(hd, KID_UP, M, [&] { return cmoe::launch_ffn_up(lo, l, h, M); }), "ffn up");
+            HIPCHK(timed(hd, KID_DOWN, M, [&] { return cmoe::launch_ffn_down(lo, l, M); }), "ffn down");
+            HIPCHK(timed(hd, KID_COMBINE, M, [&] { return cmoe::launch_combine(lo, l, y, M); }), "combine");
+        }
+    }
+    hd->t += 1;
+    if (hd->prof_left > 0) hd->prof_left -= 1;
+    return CMOE_OK;
+}
+
+cmoe_status sync_all(cmoe_handle* hd) {
+    HIPCHK(hipStreamSynchronize(hd->main), "stream synchronize");
+    if (!hd->side_is_main) HIPCHK(hipStreamSynchronize(hd->side), "stream synchronize");
+    return CMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cmoe_status cmoe_query(const cmoe_config* cfg, cmoe_sizes* out) {
+    Derived dv;
+    cmoe_status st = validate(cfg, &dv);
+    if (st != CMOE_OK) return st;
+    if (!out) return fail(CMOE_ERR_INVALID_ARG, "sizes output is NULL");
+    const Plan p = make_plan(cfg, dv);
+    out->arena_bytes = p.arena;
+    out->state_bytes = p.state_total;
+    out->workspace_bytes = p.ws_total;
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_buffers* buf, void* main_stream,
+                      void* side_stream, cmoe_handle** out) {
+    if (out) *out = nullptr;
+    Derived dv;
+    cmoe_status st = validate(cfg, &dv);
+    if (st != CMOE_OK) return st;
+    if (!w || !buf || !out) return fail(CMOE_ERR_INVALID_ARG, "weights, buffers and output handle are required");
+    if (!w->w_router || !w->w_temporal || !w->cold_pool)
+        return fail(CMOE_ERR_INVALID_ARG, "w_router, w_temporal and cold_pool are required");
+    if (cfg->mode == CMOE_MODE_SPATIO_TEMPORAL && !w->w_spatio)
+        return fail(CMOE_ERR_INVALID_ARG, "w_spatio is required in full mode");
+    if (!buf->arena || !buf->state || !buf->workspace)
+        return fail(CMOE_ERR_INVALID_ARG, "arena, state and workspace buffers are required");
+    for (const void* p : {buf->arena, buf->state, buf->workspace})
+        if (reinterpret_cast<uintptr_t>(p) & 255) return fail(CMOE_ERR_INVALID_ARG, "buffers must be 256-byte aligned");
+
+    cmoe_handle* hd = new cmoe_handle();
+    hd->cfg = *cfg;
+    hd->dv = dv;
+    hd->plan = make_plan(cfg, dv);
+    hd->R = cfg->mode == CMOE_MODE_SPATIO_TEMPORAL ? cfg->R : 0;
+    hd->main = static_cast<hipStream_t>(main_stream);
+    hd->side = side_stream ? static_cast<hipStream_t>(side_stream) : hd->main;
+    hd->side_is_main = side_stream == nullptr || side_stream == main_stream || (cfg->flags & CMOE_FLAG_FILL_ON_MAIN);
+    if (hd->side_is_main) hd->side = hd->main;
+
+    Layout& lo = hd->lo;
+    const Plan& p = hd->plan;
+    lo.L = cfg->L; lo.N = cfg->N; lo.K = cfg->K; lo.d = cfg->d; lo.F = cfg->F; lo.C = cfg->C; lo.S = cfg->S;
+    lo.mode = cfg->mode; lo.dtype = cfg->dtype; lo.NW = dv.NW; lo.n_slots = dv.n_slots; lo.n_r = dv.n_r;
+    lo.nsplit = dv.nsplit; lo.rdk = dv.rdk; lo.warmup = cfg->warmup_tokens;
+    lo.expert_elems = (int64_t)3 * cfg->d * cfg->F;
+    lo.wR = w->w_router; lo.wT = w->w_temporal; lo.wS = w->w_spatio; lo.bias = w->logit_bias; lo.pool = w->cold_pool;
+    lo.arena = buf->arena;
+    char* sb = static_cast<char*>(buf->state);
+    char* wb = static_cast<char*>(buf->workspace);
+    lo.cache = reinterpret_cast<unsigned long long*>(sb + p.cache);
+    lo.aT = reinterpret_cast<float*>(sb + p.aT);
+    lo.pS = reinterpret_cast<float*>(sb + p.pS);
+    lo.ctr = reinterpret_cast<int64_t*>(sb + p.ctr);
+    lo.phys = reinterpret_cast<int64_t*>(sb + p.phys);
+    lo.active_sum = reinterpret_cast<int64_t*>(sb + p.active_sum);
+    lo.slot_of = reinterpret_cast<int32_t*>(sb + p.slot_of);
+    lo.slot_exp = reinterpret_cast<int32_t*>(sb + p.slot_exp);
+    lo.tile_count = reinterpret_cast<uint32_t*>(sb + p.tile_count);
+    lo.n_tiles = dv.tiles;
+    lo.zpart = reinterpret_cast<double*>(wb + p.zpart);
+    lo.logits = reinterpret_cast<float*>(wb + p.logits);
+    lo.sel = reinterpret_cast<int32_t*>(wb + p.sel);
+    lo.gates = reinterpret_cast<float*>(wb + p.gates);
+    lo.events = reinterpret_cast<int32_t*>(wb + p.events);
+    lo.step_fills = reinterpret_cast<int32_t*>(wb + p.step_fills);
+    lo.fill_list = reinterpret_cast<int32_t*>(wb + p.fill_list);
+    lo.fill_count = reinterpret_cast<int32_t*>(wb + p.fill_count);
+    lo.sel_mask = reinterpret_cast<unsigned long long*>(wb + p.sel_mask);
+    lo.bcount = reinterpret_cast<int32_t*>(wb + p.bcount);
+    lo.boffset = reinterpret_cast<int32_t*>(wb + p.boffset);
+    lo.pairs = reinterpret_cast<int32_t*>(wb + p.pairs);
+    lo.active = reinterpret_cast<int32_t*>(wb + p.active);
+    lo.n_active = reinterpret_cast<int32_t*>(wb + p.n_active);
+    lo.act = wb + p.act;
+    lo.yp = reinterpret_cast<float*>(wb + p.yp);
+
+    auto mk = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
+    hd->ev_access.resize(cfg->L);
+    hd->ev_demand.resize(cfg->L);
+    hd->ev_pro.resize(cfg->L);
+    hipError_t e = mk(&hd->ev_refine0);
+    for (int l = 0; l < cfg->L && e == hipSuccess; ++l) {
+        e = mk(&hd->ev_access[l]);
+        if (e == hipSuccess) e = mk(&hd->ev_demand[l]);
+        if (e == hipSuccess) e = mk(&hd->ev_pro[l]);
+    }
+    if (e == hipSuccess) e = cmoe::launch_init(lo, hd->main);
+    if (e == hipSuccess) e = hipStreamSynchronize(hd->main);
+    if (e != hipSuccess) {
+        cmoe_destroy(hd);
+        return fail(CMOE_ERR_HIP, std::string("HIP error in cmoe_init: ") + hipGetErrorString(e));
+    }
+    *out = hd;
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_step(cmoe_handle* hd, const void* h, float* y) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    if (!h || !y) return fail(CMOE_ERR_INVALID_ARG, "h and y are required");
+    return run_token(hd, h, y, nullptr, nullptr, nullptr);
+}
+
+cmoe_status cmoe_step_logits(cmoe_handle* hd, const float* zR, const float* zT, const float* zS) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    if (!zR || !zT) return fail(CMOE_ERR_INVALID_ARG, "zR and zT are required");
+    if (hd->cfg.mode == CMOE_MODE_SPATIO_TEMPORAL && !zS) return fail(CMOE_ERR_INVALID_ARG, "zS is required in full mode");
+    return run_token(hd, nullptr, nullptr, zR, zT, zS);
+}
+
+cmoe_status cmoe_stats(cmoe_handle* hd, cmoe_stats_t* total, int64_t* per_stream_layer, int64_t* per_layer_phys) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    st = sync_all(hd);
+    if (st != CMOE_OK) return st;
+    const cmoe_config& c = hd->cfg;
+    std::vector<int64_t> ctr((size_t)c.S * c.L * cmoe::kNctr), phys((size_t)c.L * 2);
+    HIPCHK(hipMemcpy(ctr.data(), hd->lo.ctr, ctr.size() * 8, hipMemcpyDeviceToHost), "counter read");
+    HIPCHK(hipMemcpy(phys.data(), hd->lo.phys, phys.size() * 8, hipMemcpyDeviceToHost), "counter read");
+    if (per_stream_layer) std::memcpy(per_stream_layer, ctr.data(), ctr.size() * 8);
+    if (per_layer_phys) std::memcpy(per_layer_phys, phys.data(), phys.size() * 8);
+    if (total) {
+        cmoe_stats_t t{};
+        for (int s = 0; s < c.S; ++s) {
+            for (int l = 0; l < c.L; ++l) {
+                const int64_t* v = &ctr[((size_t)s * c.L + l) * cmoe::kNctr];
+                t.accesses += v[cmoe::kCtrA];
+                t.hits += v[cmoe::kCtrHits];
+                t.demand_misses += v[cmoe::kCtrD];
+                t.proactive_loads += v[cmoe::kCtrP];
+            }
+            t.tokens += ctr[((size_t)s * c.L + 0) * cmoe::kNctr + cmoe::kCtrT];
+        }
+        for (int64_t v : phys) t.phys_fills += v;
+        t.traffic_bytes = (t.demand_misses + t.proactive_loads) * (int64_t)hd->dv.expert_bytes;
+        t.phys_bytes = t.phys_fills * (int64_t)hd->dv.expert_bytes;
+        *total = t;
+    }
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_get_cache(cmoe_handle* hd, int32_t stream, int32_t layer, int32_t* experts, int32_t* n) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    if (stream < 0 || stream >= hd->cfg.S || layer < 0 || layer >= hd->cfg.L || !experts || !n)
+        return fail(CMOE_ERR_INVALID_ARG, "stream or layer out of range, or NULL output");
+    st = sync_all(hd);
+    if (st != CMOE_OK) return st;
+    uint64_t w[4] = {0, 0, 0, 0};
+    HIPCHK(hipMemcpy(w, hd->lo.cache + ((size_t)stream * hd->cfg.L + layer) * hd->dv.NW, hd->dv.NW * 8,
+                     hipMemcpyDeviceToHost),
+           "cache read");
+    int k = 0;
+    for (int e = 0; e < hd->cfg.N; ++e)
+        if ((w[e >> 6] >> (e & 63)) & 1ull) {
+            if (k < hd->cfg.C) experts[k] = e;
+            ++k;
+        }
+    *n = k;
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_set_cache(cmoe_handle* hd, int32_t stream, int32_t layer, const int32_t* experts, int32_t n) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    if (stream < 0 || stream >= hd->cfg.S || layer < 0 || layer >= hd->cfg.L)
+        return fail(CMOE_ERR_INVALID_ARG, "stream or layer out of range");
+    if (n < 0 || n > hd->cfg.C || (n > 0 && !experts)) return fail(CMOE_ERR_INVALID_ARG, "need 0 <= n <= C experts");
+    uint64_t w[4] = {0, 0, 0, 0};
+    for (int i = 0; i < n; ++i) {
+        const int e = experts[i];
+        if (e < 0 || e >= hd->cfg.N) return fail(CMOE_ERR_INVALID_ARG, "expert index out of range");
+        if ((w[e >> 6] >> (e & 63)) & 1ull) return fail(CMOE_ERR_INVALID_ARG, "duplicate expert");
+        w[e >> 6] |= 1ull << (e & 63);
+    }
+    st = sync_all(hd);
+    if (st != CMOE_OK) return st;
+    HIPCHK(hipMemcpy(hd->lo.cache + ((size_t)stream * hd->cfg.L + layer) * hd->dv.NW, w, hd->dv.NW * 8,
+                     hipMemcpyHostToDevice),
+           "cache write");
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_set_R(cmoe_handle* hd, int32_t R) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    if (R < 0 || R > hd->cfg.N) return fail(CMOE_ERR_INVALID_ARG, "R must be in [0, N]");
+    hd->R = hd->cfg.mode == CMOE_MODE_SPATIO_TEMPORAL ? R : 0;
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_reset(cmoe_handle* hd) {
+    if (!hd) return fail(CMOE_ERR_INVALID_ARG, "handle is NULL");
+    hd->broken = false;
+    (void)hipGetLastError();
+    cmoe_status st = sync_all(hd);
+    if (st != CMOE_OK) return st;
+    HIPCHK(cmoe::launch_init(hd->lo, hd->main), "reset");
+    HIPCHK(hipStreamSynchronize(hd->main), "reset");
+    hd->t = 0;
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_destroy(cmoe_handle* hd) {
+    if (!hd) return CMOE_OK;
+    if (hd->main) {
+        (void)hipStreamSynchronize(hd->main);
+        if (!hd->side_is_main) (void)hipStreamSynchronize(hd->side);
+    }
+    auto rm = [](hipEvent_t e) {
+        if (e) (void)hipEventDestroy(e);
+    };
+    rm(hd->ev_refine0);
+    for (auto e : hd->ev_access) rm(e);
+    for (auto e : hd->ev_demand) rm(e);
+    for (auto e : hd->ev_pro) rm(e);
+    for (auto e : hd->prof_pool) rm(e);
+    delete hd;
+    return CMOE_OK;
+}
+
+size_t cmoe_view_bytes(const cmoe_handle* hd, int32_t view) {
+    if (!hd) return 0;
+    const size_t S = hd->cfg.S, L = hd->cfg.L, N = hd->cfg.N, K = hd->cfg.K;
+    switch (view) {
+        case CMOE_VIEW_LOGITS: return L * S * hd->dv.n_r * N * 4;
+        case CMOE_VIEW_SELECTED: return L * S * K * 4;
+        case CMOE_VIEW_GATES: return L * S * K * 4;
+        case CMOE_VIEW_CACHE: return S * L * hd->dv.NW * 8;
+        case CMOE_VIEW_COUNTERS: return S * L * cmoe::kNctr * 8;
+        case CMOE_VIEW_PHYS: return L * 2 * 8;
+        case CMOE_VIEW_SLOTS: return L * N * 4;
+        case CMOE_VIEW_EVENTS: return L * S * 4 * 4;
+        case CMOE_VIEW_FILLS: return L * 2 * 4;
+        case CMOE_VIEW_ACTIVE: return L * 8;
+        default: return 0;
+    }
+}
+
+cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t bytes) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    const size_t need = cmoe_view_bytes(hd, view);
+    if (need == 0) return fail(CMOE_ERR_INVALID_ARG, "unknown view");
+    if (!host_out || bytes < need) return fail(CMOE_ERR_INVALID_ARG, "output buffer too small");
+    const void* src = nullptr;
+    const Layout& lo = hd->lo;
+    switch (view) {
+        case CMOE_VIEW_LOGITS: src = lo.logits; break;
+        case CMOE_VIEW_SELECTED: src = lo.sel; break;
+        case CMOE_VIEW_GATES: src = lo.gates; break;
+        case CMOE_VIEW_CACHE: src = lo.cache; break;
+        case CMOE_VIEW_COUNTERS: src = lo.ctr; break;
+        case CMOE_VIEW_PHYS: src = lo.phys; break;
+        case CMOE_VIEW_SLOTS: src = lo.slot_of; break;
+        case CMOE_VIEW_EVENTS: src = lo.events; break;
+        case CMOE_VIEW_FILLS: src = lo.step_fills; break;
+        case CMOE_VIEW_ACTIVE: src = lo.active_sum; break;
+    }
+    st = sync_all(hd);
+    if (st != CMOE_OK) return st;
+    HIPCHK(hipMemcpy(host_out, src, need, hipMemcpyDeviceToHost), "view read");
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_profile_begin(cmoe_handle* hd, int32_t max_tokens, uint32_t kernel_mask) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    if (max_tokens < 1) return fail(CMOE_ERR_INVALID_ARG, "max_tokens must be >= 1");
+    hd->prof_mask = kernel_mask ? kernel_mask : ((1u << CMOE_KERNEL_COUNT) - 1u);
+    int kinds = 0;
+    for (int k = 0; k < CMOE_KERNEL_COUNT; ++k) kinds += (hd->prof_mask >> k) & 1u;
+    const size_t per_token = ((size_t)hd->cfg.L * 2 + 2) * kinds;  // timed launches per token, upper bound
+    const size_t need = 2 * per_token * (size_t)max_tokens;
+    while (hd->prof_pool.size() < need) {
+        hipEvent_t e;
+        HIPCHK(hipEventCreate(&e), "event create");
+        hd->prof_pool.push_back(e);
+    }
+    hd->prof_rec.clear();
+    hd->prof_next = 0;
+    hd->prof_left = max_tokens;
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_profile_end(cmoe_handle* hd, double* ms_out, int64_t* launches_out) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    st = sync_all(hd);
+    if (st != CMOE_OK) return st;
+    std::vector<double> ms(CMOE_KERNEL_COUNT, 0.0);
+    std::vector<int64_t> n(CMOE_KERNEL_COUNT, 0);
+    for (const auto& r : hd->prof_rec) {
+        float v = 0.0f;
+        HIPCHK(hipEventElapsedTime(&v, hd->prof_pool[r.second], hd->prof_pool[r.second + 1]), "event elapsed");
+        ms[r.first] += v;
+        n[r.first] += 1;
+    }
+    if (ms_out) std::memcpy(ms_out, ms.data(), ms.size() * sizeof(double));
+    if (launches_out) std::memcpy(launches_out, n.data(), n.size() * sizeof(int64_t));
+    hd->prof_rec.clear();
+    hd->prof_next = 0;
+    hd->prof_left = 0;
+    return CMOE_OK;
+}
+
+const char* cmoe_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -218,3 +218,46 @@ def fill_hidden_dev(w: Workload, out_ptr: int, T: Optional[int] = None, stream: 
     rho, c0 = ar1_params(w)
     _check(_load_hip().syn_dev_ar1(w.seed, hidden_tid(0, 0), 1 << 24, 1, w.S, w.L, w.d, T, rho, c0,
                                    unit_scale(), int(w.dtype == DTYPE_BF16), out_ptr, stream), "hidden")
+
+
+def device_inputs(w: Workload, T: Optional[int] = None, with_hidden: bool = True, stream: int = 0):
+    """All inputs of a workload generated on the GPU (torch tensors on cuda:0).
+
+    Returns a dict: wR, wT, wS ([L][N][d] or None), bias ([L][N] fp32 or None),
+    pool ([L][N][3 d F] on the device, or in pinned host memory for a
+    host-pool workload) and hidden ([T][S][L][d], token-major).  Values are
+    bit-identical to the host twin's.
+    """
+    import torch
+    dt = torch.bfloat16 if w.dtype == DTYPE_BF16 else torch.float32
+    dev = torch.device("cuda", torch.cuda.current_device())
+    out = {}
+    out["wR"] = torch.empty((w.L, w.N, w.d), dtype=dt, device=dev)
+    out["wT"] = torch.empty((w.L, w.N, w.d), dtype=dt, device=dev)
+    fill_router_dev(w, KIND_ROUTER_NATIVE, out["wR"].data_ptr(), stream)
+    fill_router_dev(w, KIND_ROUTER_TEMPORAL, out["wT"].data_ptr(), stream)
+    if w.mode == MODE_SPATIO_TEMPORAL:
+        out["wS"] = torch.empty((w.L, w.N, w.d), dtype=dt, device=dev)
+        fill_router_dev(w, KIND_ROUTER_SPATIO, out["wS"].data_ptr(), stream)
+    else:
+        out["wS"] = None
+    zb = zipf_bias(w)
+    out["bias"] = None if zb is None else torch.from_numpy(zb).to(dev)
+    per = 3 * w.F * w.d
+    if w.pool_kind == POOL_HOST_PINNED:
+        pool = torch.empty((w.L, w.N, per), dtype=dt, pin_memory=True)
+        stage = torch.empty((1, w.N, per), dtype=dt, device=dev)
+        for l in range(w.L):  # generate one layer on the device, copy it to host
+            fill_pool_dev(w, stage.data_ptr(), stream, layers=(l, l + 1))
+            pool[l].copy_(stage[0])
+        del stage
+    else:
+        pool = torch.empty((w.L, w.N, per), dtype=dt, device=dev)
+        fill_pool_dev(w, pool.data_ptr(), stream)
+    out["pool"] = pool
+    if with_hidden:
+        T = w.T if T is None else T
+        out["hidden"] = torch.empty((T, w.S, w.L, w.d), dtype=dt, device=dev)
+        fill_hidden_dev(w, out["hidden"].data_ptr(), T, stream)
+    torch.cuda.synchronize()
+    return out

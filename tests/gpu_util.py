@@ -1,0 +1,49 @@
+"""Helpers shared by the GPU tests (not collected by pytest)."""
+from __future__ import annotations
+
+import copy
+import sys
+
+import numpy as np
+
+import oracle
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def clone_run(run: oracle.Run) -> oracle.Run:
+    r = copy.copy(run)
+    r.cfg = oracle._Cfg(*[getattr(run.cfg, n) for n, _ in oracle._Cfg._fields_])
+    for n in ("cache", "aT", "pS", "ctr", "slot_of", "phys"):
+        setattr(r, n, getattr(run, n).copy())
+    return r
+
+
+def compare_step(eng, run: oracle.Run, out: dict, where: str):
+    """Bit-exact comparison of every integer output of one token."""
+    from paper_2609_04895_amd import cmoe as B
+    sel = eng.cmoe_read(B.CMOE_VIEW_SELECTED)             # [L][S][K]
+    assert np.array_equal(sel.transpose(1, 0, 2), out["sel"]), f"{where}: selected experts differ"
+    gates = eng.cmoe_read(B.CMOE_VIEW_GATES).transpose(1, 0, 2)
+    assert np.allclose(gates, out["gate"], rtol=2e-6, atol=1e-7), f"{where}: gates differ"
+    cache = eng.cache_sets()
+    assert np.array_equal(cache, run.cache.astype(bool)), f"{where}: cache sets differ"
+    ev = eng.cmoe_read(B.CMOE_VIEW_EVENTS)                # [L][S][4]
+    assert np.array_equal(ev[:, :, 0].T, out["hits"]), f"{where}: hits differ"
+    assert np.array_equal(ev[:, :, 1].T, out["nD"]), f"{where}: demand misses differ"
+    assert np.array_equal(ev[:, :, 2].T, out["nP"]), f"{where}: proactive loads differ"
+    ctr = eng.cmoe_read(B.CMOE_VIEW_COUNTERS)
+    assert np.array_equal(ctr, run.ctr), f"{where}: counters differ"
+    slots = eng.cmoe_read(B.CMOE_VIEW_SLOTS)
+    assert np.array_equal(slots, run.slot_of), f"{where}: slot maps differ"
+    fills = eng.cmoe_read(B.CMOE_VIEW_FILLS)
+    assert np.array_equal(fills, out["fills"]), f"{where}: physical fills differ"
+    assert np.array_equal(eng.cmoe_read(B.CMOE_VIEW_PHYS), run.phys), f"{where}: physical counters differ"
+
+
+def rel_err(y, ref):
+    den = float(np.max(np.abs(ref)))
+    return float(np.max(np.abs(np.asarray(y, np.float64) - ref))) / (den if den > 0 else 1.0)

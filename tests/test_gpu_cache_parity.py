@@ -1,0 +1,142 @@
+"""Bit-exact parity of the cache path (softmax, Top-K, refinement, access,
+retention, counters, residency, fills) with the oracle, driven through
+cmoe_step_logits with the same fp32 logits on both sides."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import compare_step, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def make_engine(L, N, K, C, R, S, mode, warmup=0, side=True, d=64, F=64):
+    from paper_2609_04895_amd import cmoe as B
+    dev = torch.device("cuda", 0)
+    # router weights are not read by cmoe_step_logits; the pool is (fills)
+    w = torch.zeros((L, N, d), dtype=torch.float32, device=dev)
+    pool = torch.arange(L * N * 3 * d * F, dtype=torch.float32, device=dev).reshape(L, N, 3 * d * F)
+    cfg = B.make_config(L, N, K, d, F, C, R, S, mode, B.CMOE_F32, B.CMOE_POOL_DEVICE, warmup,
+                        0 if side else B.CMOE_FLAG_FILL_ON_MAIN)
+    eng = B.Engine(cfg, w, w, w if mode == 1 else None, None, pool,
+                   side_stream=torch.cuda.Stream() if side else None)
+    return eng, pool
+
+
+def logits_sequence(rng, T, S, L, N, ties):
+    """AR(1) logits [T][3][S][L][N]; with `ties` the values are rounded to
+    multiples of 1/4 so that equal logits and equal scores are frequent."""
+    z = np.empty((T, 3, S, L, N), np.float32)
+    prev = rng.normal(size=(3, S, L, N))
+    for t in range(T):
+        prev = 0.85 * prev + np.sqrt(1 - 0.85 ** 2) * rng.normal(size=prev.shape)
+        v = prev * 2.0
+        if ties:
+            v = np.round(v * 4) / 4
+        z[t] = v.astype(np.float32)
+    return z
+
+
+CASES = [
+    # L, N, K, C, R, S, mode, warmup, ties, side
+    (3, 16, 2, 6, 0, 1, 0, 0, False, True),
+    (3, 16, 2, 2, 0, 3, 0, 0, True, True),       # C = K: the cache is the last selection
+    (2, 16, 2, 16, 0, 2, 0, 0, True, False),     # C = N: only compulsory misses
+    (4, 32, 4, 8, 2, 5, 1, 0, True, True),       # GPT-OSS-like shape, full mode
+    (3, 100, 7, 20, 5, 37, 1, 2, True, True),    # ragged N and S
+    (3, 128, 8, 32, 0, 9, 1, 0, False, True),    # full mode with R = 0
+    (2, 128, 8, 32, 0, 70, 0, 1, True, True),    # Qwen3-like shape, update-only
+    (2, 256, 8, 40, 12, 6, 1, 0, True, True),    # N = 256 (four experts per lane)
+    (2, 64, 64, 64, 64, 2, 1, 0, True, False),   # K = C = N = R
+    (2, 1, 1, 1, 1, 2, 1, 0, False, True),       # a single expert
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"L{c[0]}N{c[1]}K{c[2]}C{c[3]}R{c[4]}S{c[5]}m{c[6]}" for c in CASES])
+def test_cache_path_bit_exact(case):
+    L, N, K, C, R, S, mode, warmup, ties, side = case
+    say(f"cache parity case {case}")
+    T = 20
+    rng = np.random.default_rng(hash(case) % (2 ** 32))
+    z = logits_sequence(rng, T, S, L, N, ties)
+    eng, _ = make_engine(L, N, K, C, R, S, mode, warmup, side)
+    run = oracle.Run(L, N, K, C, R, S, mode, warmup)
+    dev = torch.device("cuda", 0)
+    for t in range(T):
+        zR, zT, zS = (torch.from_numpy(z[t, i]).to(dev) for i in range(3))
+        eng.cmoe_step_logits(zR, zT, zS if mode == 1 else None)
+        out = run.step(z[t, 0], z[t, 1], z[t, 2] if mode == 1 else None, want="all")
+        compare_step(eng, run, out, f"case {case} token {t}")
+    total, per, phys = eng.cmoe_stats()
+    ref = run.totals()
+    for k in ("accesses", "hits", "demand_misses", "proactive_loads", "tokens", "phys_fills"):
+        assert total[k] == ref[k], k
+    assert total["hits"] + total["demand_misses"] == total["accesses"]
+    assert total["traffic_bytes"] == (total["demand_misses"] + total["proactive_loads"]) * 3 * 64 * 64 * 4
+    if mode == 0 or R == 0:
+        assert total["proactive_loads"] == 0
+    eng.cmoe_destroy()
+
+
+def test_refinement_budget_change_and_cache_set_replay():
+    """R changes between tokens (no retraining needed, Section 3.3) and a
+    cache set from the host are followed identically by both sides."""
+    L, N, K, C, S = 3, 32, 4, 8, 4
+    rng = np.random.default_rng(5)
+    z = logits_sequence(rng, 16, S, L, N, ties=True)
+    eng, _ = make_engine(L, N, K, C, 2, S, 1)
+    run = oracle.Run(L, N, K, C, 2, S, 1)
+    dev = torch.device("cuda", 0)
+    for t in range(16):
+        if t == 5:
+            eng.cmoe_set_R(6)
+            run.set_R(6)
+        if t == 9:
+            eng.cmoe_set_R(0)
+            run.set_R(0)
+        if t == 12:
+            eng.cmoe_set_cache(1, 2, [3, 7, 30])
+            run.cache[1, 2, :] = 0
+            run.cache[1, 2, [3, 7, 30]] = 1
+            assert eng.cmoe_get_cache(1, 2) == [3, 7, 30]
+        zR, zT, zS = (torch.from_numpy(z[t, i]).to(dev) for i in range(3))
+        eng.cmoe_step_logits(zR, zT, zS)
+        out = run.step(z[t, 0], z[t, 1], z[t, 2], want="all")
+        compare_step(eng, run, out, f"token {t}")
+    for s in range(S):
+        for l in range(L):
+            assert eng.cmoe_get_cache(s, l) == sorted(np.nonzero(run.cache[s, l])[0].tolist())
+    # reset returns to an empty state and a fresh replay matches again
+    eng.cmoe_reset()
+    run = oracle.Run(L, N, K, C, 0, S, 1)
+    for t in range(4):
+        zR, zT, zS = (torch.from_numpy(z[t, i]).to(dev) for i in range(3))
+        eng.cmoe_step_logits(zR, zT, zS)
+        out = run.step(z[t, 0], z[t, 1], z[t, 2], want="all")
+        compare_step(eng, run, out, f"after reset, token {t}")
+    eng.cmoe_destroy()
+
+
+def test_fills_copy_the_right_expert_bytes():
+    """Arena slots hold exactly the cold-pool bytes of the expert mapped there."""
+    L, N, K, C, S = 2, 16, 2, 4, 3
+    rng = np.random.default_rng(8)
+    z = logits_sequence(rng, 6, S, L, N, ties=False)
+    eng, pool = make_engine(L, N, K, C, 2, S, 1)
+    dev = torch.device("cuda", 0)
+    for t in range(6):
+        zR, zT, zS = (torch.from_numpy(z[t, i]).to(dev) for i in range(3))
+        eng.cmoe_step_logits(zR, zT, zS)
+    from paper_2609_04895_amd import cmoe as B
+    slots = eng.cmoe_read(B.CMOE_VIEW_SLOTS)
+    n_slots = min(N, S * C)
+    per = 3 * 64 * 64
+    arena = eng.arena[: L * n_slots * per * 4].view(torch.float32).reshape(L, n_slots, per)
+    for l in range(L):
+        for e in range(N):
+            q = int(slots[l, e])
+            if q >= 0:
+                assert torch.equal(arena[l, q], pool[l, e]), (l, e, q)
+    eng.cmoe_destroy()

@@ -1,0 +1,157 @@
+"""End-to-end parity of cmoe_step (router GEMV, cache path, fills, expert FFN)
+with the oracle on the same seeded inputs.
+
+- The device generator reproduces the host twin's tensors bit for bit.
+- Router logits: the GPU's fp32 logits equal the oracle's (fp64 sum rounded
+  once) except possibly for sums within an fp32 rounding boundary; any
+  difference is at most one ulp and is counted.
+- Decisions: the oracle replayed on the GPU's own logits matches every
+  selection, cache set and counter bit for bit; decisions from the oracle's
+  own logits may differ only where a Top-K logit gap is below 1e-6.
+- FFN outputs: max-norm relative error <= 1e-5 (fp32) or 2e-2 (bf16, fp32
+  accumulation) against the oracle's fp64 SwiGLU on the same selection.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import clone_run, compare_step, rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def bf16_bits(t):
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def f32_of(w, t):
+    """Device tensor -> float32 numpy of the stored values."""
+    if w.dtype == synth.DTYPE_BF16:
+        return (bf16_bits(t).astype(np.uint32) << 16).view(np.float32)
+    return t.cpu().numpy()
+
+
+def test_device_generator_matches_host_twin():
+    for name, w in (("tiny", synth.WORKLOADS["tiny"]),
+                    ("small_bf16", synth.WORKLOADS["gptoss_20b"].replace(L=2, S=3, d=256, F=128))):
+        say(f"generator twin {name}")
+        inp = synth.device_inputs(w, T=7)
+        for kind, key in ((synth.KIND_ROUTER_NATIVE, "wR"), (synth.KIND_ROUTER_TEMPORAL, "wT")):
+            for l in range(w.L):
+                assert np.array_equal(f32_of(w, inp[key][l]), synth.router_host(w, kind, l))
+        for l, e in ((0, 0), (w.L - 1, w.N - 1), (0, w.N // 2)):
+            g, u, dn = synth.expert_host(w, l, e)
+            dev = f32_of(w, inp["pool"][l, e])
+            fd = w.F * w.d
+            assert np.array_equal(dev[:fd], g.ravel()) and np.array_equal(dev[fd:2 * fd], u.ravel())
+            assert np.array_equal(dev[2 * fd:], dn.ravel())
+        for s in range(w.S):
+            for l in range(w.L):
+                ref = synth.hidden_host(w, s, l, T=7)
+                assert np.array_equal(f32_of(w, inp["hidden"][:, s, l]), ref)
+        del inp
+
+
+def run_e2e(w, T, tol, check_ffn_every=1, samples=None):
+    from paper_2609_04895_amd import cmoe as B
+    from paper_2609_04895_amd.workload import engine_for
+    inp = synth.device_inputs(w, T=T)
+    eng = engine_for(w, inp)
+    dev = torch.device("cuda", 0)
+    y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device=dev)
+    full = w.mode == synth.MODE_SPATIO_TEMPORAL
+    n_r = 3 if full else 2
+    # host copies of what the oracle needs
+    WR = [synth.router_host(w, synth.KIND_ROUTER_NATIVE, l) for l in range(w.L)]
+    WT = [synth.router_host(w, synth.KIND_ROUTER_TEMPORAL, l) for l in range(w.L)]
+    WS = [synth.router_host(w, synth.KIND_ROUTER_SPATIO, l) for l in range(w.L)] if full else None
+    bias = synth.zipf_bias(w)
+    H = {(s, l): synth.hidden_host(w, s, l, T=T) for s in range(w.S) for l in range(w.L)}
+    experts = {}
+
+    def expert(l, e):
+        l, e = int(l), int(e)
+        if (l, e) not in experts:
+            experts[(l, e)] = synth.expert_host(w, l, e)
+        return experts[(l, e)]
+
+    run = oracle.Run(w.L, w.N, w.K, w.C, w.R, w.S, w.mode)
+    ulp_diffs = 0
+    near_ties = 0
+    worst_ffn = 0.0
+    for t in range(T):
+        eng.cmoe_step(inp["hidden"][t], y)
+        z_gpu = eng.cmoe_read(B.CMOE_VIEW_LOGITS)      # [L][S][n_r][N]
+        # oracle logits from the host twin's inputs
+        z_orc = np.empty((w.S, w.L, n_r, w.N), np.float32)
+        for s in range(w.S):
+            for l in range(w.L):
+                h = H[(s, l)][t]
+                z_orc[s, l, 0] = oracle.logits(WR[l], h, None if bias is None else bias[l])
+                z_orc[s, l, 1] = oracle.logits(WT[l], h)
+                if full:
+                    z_orc[s, l, 2] = oracle.logits(WS[l], h)
+        zg = z_gpu.transpose(1, 0, 2, 3)
+        diff = zg != z_orc
+        if diff.any():
+            gap = np.abs(zg.astype(np.float64) - z_orc.astype(np.float64))
+            assert np.all(gap <= np.spacing(np.abs(z_orc)) * 1.0001), "logit differs by more than one ulp"
+            ulp_diffs += int(diff.sum())
+        # step-local: decisions from the oracle's own logits vs the GPU's
+        own = clone_run(run).step(z_orc[:, :, 0], z_orc[:, :, 1], z_orc[:, :, 2] if full else None, want="all")
+        out = run.step(zg[:, :, 0], zg[:, :, 1], zg[:, :, 2] if full else None, want="all")
+        compare_step(eng, run, out, f"{w.name} token {t}")
+        if not np.array_equal(own["sel"], out["sel"]):
+            for s, l in zip(*np.nonzero((own["sel"] != out["sel"]).any(axis=-1))):
+                zs = np.sort(z_orc[s, l, 0].astype(np.float64))[::-1]
+                assert zs[w.K - 1] - zs[w.K] < 1e-6, "selection differs without a near tie"
+                near_ties += 1
+        # FFN
+        if t % check_ffn_every == 0:
+            yg = y.cpu().numpy()
+            pairs = samples if samples is not None else [(s, l) for s in range(w.S) for l in range(w.L)]
+            for s, l in pairs:
+                sel = out["sel"][s, l]
+                Wg = np.stack([expert(l, e)[0] for e in sel])
+                Wu = np.stack([expert(l, e)[1] for e in sel])
+                Wd = np.stack([expert(l, e)[2] for e in sel])
+                ref = oracle.moe_ffn(Wg, Wu, Wd, out["gate"][s, l], H[(s, l)][t])
+                err = rel_err(yg[s, l], ref)
+                worst_ffn = max(worst_ffn, err)
+                assert err <= tol, f"token {t} stream {s} layer {l}: FFN relative error {err}"
+    say(f"{w.name}: logits differing by one ulp: {ulp_diffs}; near-tie selection flips: {near_ties}; "
+        f"worst FFN error {worst_ffn:.3g}")
+    tot, _, _ = eng.cmoe_stats()
+    ref = run.totals()
+    for k in ("accesses", "hits", "demand_misses", "proactive_loads", "tokens", "phys_fills"):
+        assert tot[k] == ref[k], k
+    eng.cmoe_destroy()
+    del inp
+
+
+def test_tiny_fp32_workload_end_to_end():
+    """L=4, N=16, K=2, d=256, F=512, C=6, update-only, 1 stream x 256 tokens."""
+    run_e2e(synth.WORKLOADS["tiny"], T=256, tol=1e-5)
+
+
+def test_bf16_full_mode_small_shape():
+    w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_small", L=3, d=256, F=128, S=20, C=32, R=4,
+                                             mode=synth.MODE_SPATIO_TEMPORAL)
+    run_e2e(w, T=10, tol=2e-2)
+
+
+def test_bf16_ragged_chunks_and_zipf_bias():
+    # d = 320 and F = 192 are not multiples of 256: exercises the chunk tails;
+    # many tokens per expert (N = 16, S = 40) exercises several token groups
+    w = synth.WORKLOADS["qwen3_30b_zipf"].replace(name="bf16_ragged", L=2, N=16, K=4, d=320, F=192, S=40, C=6,
+                                                  R=2)
+    run_e2e(w, T=6, tol=2e-2)
+
+
+def test_bf16_update_only_gptoss_like():
+    w = synth.WORKLOADS["gptoss_20b"].replace(name="gptoss_small", L=2, d=192, F=192, S=7,
+                                              mode=synth.MODE_TEMPORAL, R=0)
+    run_e2e(w, T=8, tol=2e-2)
