@@ -64,7 +64,9 @@ typedef enum {
 } cmoe_pool_kind;
 
 /* flags */
-#define CMOE_FLAG_FILL_ON_MAIN 0x1u /* run all fills on the main stream          */
+#define CMOE_FLAG_FILL_ON_MAIN 0x1u /* run proactive fills on the main stream too
+                                       (demand fills always run there: they gate
+                                       the layer's FFN)                          */
 
 /* Problem shape.  Valid values: 1 <= K <= C <= N (Section 2: capacity at least
  * Top-K); 0 <= R <= N; L, S >= 1; d, F >= 1; warmup_tokens >= 0.  Supported:
@@ -206,10 +208,11 @@ cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t byte
  * kernels selected by kernel_mask (bit i = kernel id i; 0 selects all);
  * cmoe_profile_end synchronizes and returns, per kernel id, the summed
  * milliseconds and the launch count.  Kernel ids: 0 router GEMV, 1 cache
- * step, 2 residency and expert grouping, 3 expert gate/up, 4 expert down,
- * 5 combine, 6 fill.  ms_out and launches_out hold CMOE_KERNEL_COUNT entries.
- * Event pairs add work between launches; time few kernels at once. */
-#define CMOE_KERNEL_COUNT 7
+ * step (routing, refinement, retention, counters, expert grouping),
+ * 2 residency and fill, 3 expert gate/up, 4 expert down, 5 combine.
+ * ms_out and launches_out hold CMOE_KERNEL_COUNT entries.  Event pairs add
+ * work between launches; time few kernels at once. */
+#define CMOE_KERNEL_COUNT 6
 cmoe_status cmoe_profile_begin(cmoe_handle* hd, int32_t max_tokens, uint32_t kernel_mask);
 cmoe_status cmoe_profile_end(cmoe_handle* hd, double* ms_out, int64_t* launches_out);
 

@@ -40,8 +40,8 @@ CMOE_VIEW_SLOTS = 6
 CMOE_VIEW_EVENTS = 7
 CMOE_VIEW_FILLS = 8
 CMOE_VIEW_ACTIVE = 9
-CMOE_KERNEL_COUNT = 7
-KERNEL_NAMES = ("router", "cache_step", "residency", "ffn_up", "ffn_down", "combine", "fill")
+CMOE_KERNEL_COUNT = 6
+KERNEL_NAMES = ("router", "cache_step", "fill", "ffn_up", "ffn_down", "combine")
 
 EXPORTED = ("cmoe_query", "cmoe_init", "cmoe_step", "cmoe_step_logits", "cmoe_stats", "cmoe_get_cache",
             "cmoe_set_cache", "cmoe_set_R", "cmoe_reset", "cmoe_destroy", "cmoe_view_bytes", "cmoe_read",

@@ -23,11 +23,10 @@
 // refine-only launch at the start of the token, from the previous token's
 // last-layer p^S (the wrap-around of the causal predecessor).
 //
-// finish_kernel (one workgroup): for a layer whose caches changed, makes the
-// HBM slots hold the union of the streams' caches (experts that left free
-// their slots; each new expert, ascending, takes the lowest free slot and is
-// queued for a copy from the cold pool), and groups the layer's (stream, k)
-// selections by expert for the FFN.
+// The same kernel groups the layer's (stream, k) selections by expert for the
+// FFN (fixed-capacity buckets filled with integer atomics) and counts the
+// distinct experts executed.  Physical residency is handled by the fill
+// kernel.
 //
 // Fixed fp32 softmax: m = max z; u_e = exp(z_e - m) with the exponential
 // below; the sum is a strided halving over the next power of two P >= N
@@ -279,9 +278,19 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
                         const float* src = r == 0 ? a.zR : (r == 1 ? a.zT : a.zS);
                         v = src[sl * N + e];
                     } else {
-                        v = lo.logits[(((int64_t)l * lo.S + s) * lo.n_r + r) * N + e];  // router output
+                        // router splits of this logit, added in ascending split order
+                        const double* zp = lo.zpart + (((int64_t)s * lo.n_r + r) * N + e) * lo.nsplit;
+                        double pv[kMaxSplit];
+#pragma unroll
+                        for (int p = 0; p < kMaxSplit; ++p) pv[p] = p < lo.nsplit ? zp[p] : 0.0;
+                        double acc = 0.0;
+#pragma unroll
+                        for (int p = 0; p < kMaxSplit; ++p)
+                            if (p < lo.nsplit) acc += pv[p];
+                        if (r == 0 && lo.bias) acc += (double)lo.bias[(int64_t)l * N + e];
+                        v = (float)acc;
                     }
-                    if (a.flags & kFlagInject) lo.logits[(((int64_t)l * lo.S + s) * lo.n_r + r) * N + e] = v;
+                    lo.logits[(((int64_t)l * lo.S + s) * lo.n_r + r) * N + e] = v;
                 }
                 z[r][j] = v;
             }
@@ -329,6 +338,13 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             const int64_t o = ((int64_t)l * lo.S + s) * K + lane;
             lo.sel[o] = my_sel;
             lo.gates[o] = my_p / gsum;
+            // token (s, k) joins the bucket of its expert; the position inside
+            // the bucket does not affect any result (each token is its own
+            // column of the expert's matrix products)
+            const int64_t be = (int64_t)a.bbuf * N + my_sel;
+            const int pos = atomicAdd(&lo.bcount[be], 1);
+            lo.pairs[be * lo.S + pos] = (s << 8) | lane;
+            if (pos == 0 && counted) atomicAdd(&lo.active_sum[l], 1ull);
         }
         float sT[NPL];
 #pragma unroll
@@ -367,10 +383,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             }
         }
         if (lane == 0) {
-            for (int j = 0; j < lo.NW; ++j) {
-                cptr[j] = cw[j];
-                lo.sel_mask[(int64_t)s * lo.NW + j] = sw[j];
-            }
+            for (int j = 0; j < lo.NW; ++j) cptr[j] = cw[j];
             int32_t* ev = lo.events + ((int64_t)l * lo.S + s) * 4;
             ev[0] = hits;
             ev[1] = nD;
@@ -409,180 +422,12 @@ template <int NPL>
 __global__ __launch_bounds__(256) void cache_step_kernel(Layout lo, StepArgs a) {
     const int lane = threadIdx.x & 63;
     const int s = blockIdx.x * kStreamsPerBlock + (threadIdx.x >> 6);
+    if ((a.flags & kFlagAccess) && blockIdx.x == 0) {
+        // the other bucket buffer was used by the previous layer step (its FFN
+        // has completed) and is filled by the next one
+        for (int i = threadIdx.x; i < lo.N; i += blockDim.x) lo.bcount[(int64_t)(a.bbuf ^ 1) * lo.N + i] = 0;
+    }
     if (s < lo.S) stream_step<NPL>(lo, a, s, lane);  // wave-uniform branch
-}
-
-// ---------------------------------------------------------------- finish
-// Exclusive prefix sum over the 256 threads of the block; *total gets the sum.
-__device__ int block_scan(int v, int* total, int* lds4) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
-    if (lane == 63) lds4[w] = x;
-    __syncthreads();
-    int off = 0, tot = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        if (i < w) off += lds4[i];
-        tot += lds4[i];
-    }
-    __syncthreads();
-    *total = tot;
-    return off + x - v;
-}
-
-// Staged inputs of finish_kernel in (dynamic) LDS; sizes from finish_lds_bytes.
-struct FinishLds {
-    unsigned long long* cw_a;  // [S][NW] caches of the accessed layer after retention
-    unsigned long long* cw_r;  // [S][NW] caches of the refined layer
-    unsigned long long* selm;  // [S][NW] selection masks of the accessed layer
-    int* ssel;                 // [S][K]  selection lists of the accessed layer
-    int* so_a;                 // [N]     slot of each expert, accessed layer
-    int* se_a;                 // [n_slots]
-    int* so_r;                 // [N]     refined layer
-    int* se_r;                 // [n_slots]
-};
-
-__device__ FinishLds carve(const Layout& lo, unsigned char* base) {
-    FinishLds f;
-    const size_t w = (size_t)lo.S * lo.NW * 8;
-    f.cw_a = reinterpret_cast<unsigned long long*>(base);
-    f.cw_r = reinterpret_cast<unsigned long long*>(base + w);
-    f.selm = reinterpret_cast<unsigned long long*>(base + 2 * w);
-    f.ssel = reinterpret_cast<int*>(base + 3 * w);
-    f.so_a = f.ssel + (size_t)lo.S * lo.K;
-    f.se_a = f.so_a + lo.N;
-    f.so_r = f.se_a + lo.n_slots;
-    f.se_r = f.so_r + lo.N;
-    return f;
-}
-
-// Residency event of one layer from the staged caches and slot maps: the
-// layer's slots must hold the union U of the streams' caches.  Experts that
-// left U free their slot; each new expert (ascending) takes the lowest free
-// slot and is queued for a copy from the cold pool.
-__device__ void residency(const Layout& lo, int layer, int kind, bool counted, const unsigned long long* cw,
-                          int* so, int* se) {
-    __shared__ unsigned long long U[4];
-    __shared__ int free_list[kMaxN];
-    __shared__ int lds4[4];
-    const int tid = threadIdx.x;
-    if (tid < 4) U[tid] = 0ull;
-    __syncthreads();
-    for (int i = tid; i < lo.S * lo.NW; i += blockDim.x) {
-        const unsigned long long w = cw[i];
-        if (w) atomicOr(&U[i % lo.NW], w);
-    }
-    __syncthreads();
-    const int e = tid;
-    const bool inU = e < lo.N && ((U[e >> 6] >> (e & 63)) & 1ull);
-    int cur = e < lo.N ? so[e] : -1;
-    if (e < lo.N && cur >= 0 && !inU) {  // left every cache: free its slot
-        se[cur] = -1;
-        so[e] = -1;
-        cur = -1;
-    }
-    __syncthreads();
-    const bool enter = e < lo.N && inU && cur < 0;
-    const bool is_free = tid < lo.n_slots && se[tid] == -1;
-    int nfree, nenter;
-    const int rf = block_scan(is_free ? 1 : 0, &nfree, lds4);
-    if (is_free) free_list[rf] = tid;
-    const int re = block_scan(enter ? 1 : 0, &nenter, lds4);
-    __syncthreads();
-    if (enter) {  // rank re among new experts takes the rank-re free slot
-        const int q = free_list[re];
-        so[e] = q;
-        se[q] = e;
-        int32_t* fl = lo.fill_list + (((int64_t)layer * 2 + kind) * lo.N + re) * 2;
-        fl[0] = e;
-        fl[1] = q;
-    }
-    __syncthreads();
-    if (e < lo.N) lo.slot_of[(int64_t)layer * lo.N + e] = so[e];
-    if (tid < lo.n_slots) lo.slot_exp[(int64_t)layer * lo.n_slots + tid] = se[tid];
-    if (tid == 0) {
-        lo.fill_count[layer * 2 + kind] = nenter;
-        lo.step_fills[layer * 2 + kind] = nenter;
-        if (counted) lo.phys[layer * 2 + kind] += nenter;
-    }
-}
-
-// Groups the layer's (stream, k) selections by expert: per expert the token
-// count, the first bucket position (exclusive scan over experts), the active
-// expert list, and the bucket entries (stream << 8) | k in ascending stream
-// order.  Thread e handles expert e, reading the staged masks and lists.
-__device__ void buckets(const Layout& lo, int l, bool counted, const unsigned long long* selm, const int* ssel) {
-    __shared__ int lds4[4];
-    const int e = threadIdx.x;
-    const int NW = lo.NW, K = lo.K;
-    int cnt = 0;
-    if (e < lo.N)
-        for (int s = 0; s < lo.S; ++s) cnt += (int)((selm[s * NW + (e >> 6)] >> (e & 63)) & 1ull);
-    int total, nact;
-    const int off = block_scan(cnt, &total, lds4);
-    const int ra = block_scan(cnt > 0 ? 1 : 0, &nact, lds4);
-    if (e < lo.N) {
-        lo.bcount[e] = cnt;
-        lo.boffset[e] = off;
-        if (cnt > 0) lo.active[ra] = e;
-    }
-    if (threadIdx.x == 0) {
-        *lo.n_active = nact;
-        if (counted) lo.active_sum[l] += nact;
-    }
-    if (e < lo.N && cnt > 0) {
-        int pos = off;
-        for (int s = 0; s < lo.S; ++s) {
-            if ((selm[s * NW + (e >> 6)] >> (e & 63)) & 1ull) {
-                int k = 0;  // rank of e in the stream's selection (it is one of the K)
-                for (int kk = 0; kk < K; ++kk)
-                    if (ssel[s * K + kk] == e) k = kk;
-                lo.pairs[pos++] = (s << 8) | k;
-            }
-        }
-    }
-}
-
-__global__ __launch_bounds__(256) void finish_kernel(Layout lo, StepArgs a) {
-    extern __shared__ unsigned char finish_lds[];
-    const FinishLds f = carve(lo, finish_lds);
-    const bool counted = (a.flags & kFlagCount) != 0;
-    const bool acc = (a.flags & kFlagAccess) != 0, ref = (a.flags & kFlagRefine) != 0;
-    const int tid = threadIdx.x;
-    // one parallel staging phase: every input of the kernel into LDS
-    const int nw = lo.S * lo.NW;
-    for (int i = tid; i < nw; i += blockDim.x) {
-        const int s = i / lo.NW, j = i - s * lo.NW;
-        if (acc) {
-            f.cw_a[i] = lo.cache[((int64_t)s * lo.L + a.l) * lo.NW + j];
-            f.selm[i] = lo.sel_mask[i];
-        }
-        if (ref) f.cw_r[i] = lo.cache[((int64_t)s * lo.L + a.rl) * lo.NW + j];
-    }
-    if (acc)
-        for (int i = tid; i < lo.S * lo.K; i += blockDim.x) f.ssel[i] = lo.sel[(int64_t)a.l * lo.S * lo.K + i];
-    if (tid < lo.N) {
-        if (acc) f.so_a[tid] = lo.slot_of[(int64_t)a.l * lo.N + tid];
-        if (ref) f.so_r[tid] = lo.slot_of[(int64_t)a.rl * lo.N + tid];
-    }
-    if (tid < lo.n_slots) {
-        if (acc) f.se_a[tid] = lo.slot_exp[(int64_t)a.l * lo.n_slots + tid];
-        if (ref) f.se_r[tid] = lo.slot_exp[(int64_t)a.rl * lo.n_slots + tid];
-    }
-    __syncthreads();
-    if (acc) {
-        residency(lo, a.l, 0, counted, f.cw_a, f.so_a, f.se_a);
-        __syncthreads();
-        buckets(lo, a.l, counted, f.selm, f.ssel);
-        if (tid == 0 && !(a.flags & kFlagRefinedHere)) lo.step_fills[a.l * 2 + 1] = 0;
-        __syncthreads();
-    }
-    if (ref) residency(lo, a.rl, 1, counted, f.cw_r, f.so_r, f.se_r);
 }
 
 // ---------------------------------------------------------------- init
@@ -598,13 +443,12 @@ __global__ void init_kernel(Layout lo) {
     for (int64_t i = gid; i < (int64_t)lo.L * 2; i += gs) {
         lo.phys[i] = 0;
         lo.step_fills[i] = 0;
-        if (i < lo.L) lo.active_sum[i] = 0;
-        lo.fill_count[i] = 0;
     }
-    for (int64_t i = gid; i < (int64_t)lo.L * lo.N; i += gs) lo.slot_of[i] = -1;
-    for (int64_t i = gid; i < (int64_t)lo.L * lo.n_slots; i += gs) lo.slot_exp[i] = -1;
+    for (int64_t i = gid; i < lo.L; i += gs) lo.active_sum[i] = 0ull;
+    for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.N; i += gs) lo.slot_of[i] = -1;
+    for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.n_slots; i += gs) lo.slot_exp[i] = -1;
     for (int64_t i = gid; i < (int64_t)lo.L * lo.S * 4; i += gs) lo.events[i] = 0;
-    for (int64_t i = gid; i < lo.n_tiles; i += gs) lo.tile_count[i] = 0u;
+    for (int64_t i = gid; i < (int64_t)2 * lo.N; i += gs) lo.bcount[i] = 0;
 }
 
 }  // namespace
@@ -622,15 +466,6 @@ hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st
         hipLaunchKernelGGL(cache_step_kernel<2>, grid, dim3(256), 0, st, lo, a);
     else
         hipLaunchKernelGGL(cache_step_kernel<4>, grid, dim3(256), 0, st, lo, a);
-    return hipGetLastError();
-}
-
-size_t finish_lds_bytes(const Layout& lo) {
-    return (size_t)lo.S * lo.NW * 8 * 3 + (size_t)lo.S * lo.K * 4 + (size_t)(lo.N + lo.n_slots) * 2 * 4;
-}
-
-hipError_t launch_finish(const Layout& lo, const StepArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL(finish_kernel, dim3(1), dim3(256), finish_lds_bytes(lo), st, lo, a);
     return hipGetLastError();
 }
 

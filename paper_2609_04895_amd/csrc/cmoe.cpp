@@ -1,6 +1,17 @@
 // cmoe.cpp - host side of the C ABI declared in include/cmoe.h: validation,
 // buffer carving, the per-token launch sequence on the main and side streams,
 // counters, inspection and kernel timing.
+//
+// Launch sequence of one token (layers in causal order):
+//   [full mode, t >= 1, R > 0] main: cache step refining layer 0 from the
+//       previous token's last-layer Spatio prediction; side: fill (proactive)
+//   for each layer l:
+//     main: router GEMV(l)
+//     main: [wait for the proactive fill of l] cache step(l): access, retention,
+//           counters, buckets; in full mode also refinement of layer l + 1
+//     main: fill(l, demand)  -- gates the FFN of this layer
+//     side: [full mode] fill(l + 1, proactive), overlapping the FFN of l
+//     main: expert gate/up(l), expert down(l), combine(l)
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -12,6 +23,7 @@
 #include "../../include/cmoe.h"
 #include "cmoe_internal.h"
 
+using cmoe::FillArgs;
 using cmoe::Layout;
 using cmoe::StepArgs;
 
@@ -26,10 +38,10 @@ cmoe_status fail(cmoe_status st, const std::string& msg) {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-enum KernelId { KID_ROUTER = 0, KID_CACHE = 1, KID_FINISH = 2, KID_UP = 3, KID_DOWN = 4, KID_COMBINE = 5, KID_FILL = 6 };
+enum KernelId { KID_ROUTER = 0, KID_CACHE = 1, KID_FILL = 2, KID_UP = 3, KID_DOWN = 4, KID_COMBINE = 5 };
 
 struct Derived {
-    int NW, n_r, n_slots, nsplit, rdk, tiles;
+    int NW, n_r, n_slots, nsplit, rdk;
     size_t esz, expert_bytes;
 };
 
@@ -47,7 +59,7 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
         return fail(CMOE_ERR_INVALID_ARG, "unknown pool kind");
     if (c->warmup_tokens < 0) return fail(CMOE_ERR_INVALID_ARG, "warmup_tokens must be >= 0");
     if (c->N > cmoe::kMaxN) return fail(CMOE_ERR_UNSUPPORTED, "N > 256 is not supported");
-    if (c->K > 64) return fail(CMOE_ERR_UNSUPPORTED, "K > 64 is not supported");
+    if (c->K > cmoe::kMaxK) return fail(CMOE_ERR_UNSUPPORTED, "K > 64 is not supported");
     if (c->d % 64 || c->F % 64) return fail(CMOE_ERR_UNSUPPORTED, "d and F must be multiples of 64");
     if ((int64_t)c->S * c->K >= (int64_t)1 << 23) return fail(CMOE_ERR_UNSUPPORTED, "S*K too large");
     dv->NW = (c->N + 63) / 64;
@@ -55,30 +67,21 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     dv->n_slots = (int)std::min<int64_t>(c->N, (int64_t)c->S * c->C);
     dv->esz = c->dtype == CMOE_BF16 ? 2 : 4;
     dv->expert_bytes = (size_t)3 * c->d * c->F * dv->esz;
-    // router split-K: enough wavefronts to cover the chip, 32-aligned chunks
+    // router split-K: 32-aligned chunks, at most kMaxSplit splits, as few as
+    // still give about a thousand wavefronts
     const int64_t tiles = (int64_t)dv->n_r * ((c->N + 15) / 16) * ((c->S + 15) / 16);
-    if (tiles > (1 << 30)) return fail(CMOE_ERR_UNSUPPORTED, "too many router tiles");
-    dv->tiles = (int)tiles;
     int rdk = 32;
-    for (int cand : {256, 128, 64, 32}) {
-        if (tiles * ((c->d + cand - 1) / cand) >= 1024) {
-            rdk = cand;
-            break;
-        }
-    }
-    dv->rdk = std::min(rdk, c->d);
-    dv->nsplit = (c->d + dv->rdk - 1) / dv->rdk;
-    // the residency kernel stages the caches and selections of all streams in LDS
-    const size_t lds = (size_t)c->S * dv->NW * 24 + (size_t)c->S * c->K * 4 + (size_t)(c->N + dv->n_slots) * 8;
-    if (lds > cmoe::kMaxFinishLds) return fail(CMOE_ERR_UNSUPPORTED, "S * (24 ceil(N/64) + 4 K) too large");
+    while (rdk < c->d && (c->d + rdk - 1) / rdk > cmoe::kMaxSplit) rdk *= 2;
+    while (rdk * 2 <= c->d && tiles * ((c->d + 2 * rdk - 1) / (2 * rdk)) >= 1024) rdk *= 2;
+    dv->rdk = rdk;
+    dv->nsplit = (c->d + rdk - 1) / rdk;
     return CMOE_OK;
 }
 
 // Offsets of every sub-buffer; used both for sizing and for carving.
 struct Plan {
-    size_t cache, aT, pS, ctr, phys, active_sum, slot_of, slot_exp, tile_count, state_total;
-    size_t zpart, logits, sel, gates, events, step_fills, fill_list, fill_count, sel_mask, bcount, boffset,
-        pairs, active, n_active, act, yp, ws_total;
+    size_t cache, aT, pS, ctr, phys, active_sum, slot_of, slot_exp, state_total;
+    size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, ws_total;
     size_t arena;
 };
 
@@ -97,25 +100,18 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.ctr = take(S * L * cmoe::kNctr * 8);
     p.phys = take(L * 2 * 8);
     p.active_sum = take(L * 8);
-    p.slot_of = take(L * N * 4);
-    p.slot_exp = take(L * (size_t)dv.n_slots * 4);
-    p.tile_count = take((size_t)dv.tiles * 4);
+    p.slot_of = take(2 * L * N * 4);
+    p.slot_exp = take(2 * L * (size_t)dv.n_slots * 4);
     p.state_total = o;
     o = 0;
-    p.zpart = take((size_t)dv.tiles * dv.nsplit * 256 * 8);
+    p.zpart = take(S * dv.n_r * N * (size_t)dv.nsplit * 8);
     p.logits = take(L * S * dv.n_r * N * 4);
     p.sel = take(L * S * K * 4);
     p.gates = take(L * S * K * 4);
     p.events = take(L * S * 4 * 4);
     p.step_fills = take(L * 2 * 4);
-    p.fill_list = take(L * 2 * N * 2 * 4);
-    p.fill_count = take(L * 2 * 4);
-    p.sel_mask = take(S * dv.NW * 8);
-    p.bcount = take(N * 4);
-    p.boffset = take(N * 4);
-    p.pairs = take(S * K * 4);
-    p.active = take(N * 4);
-    p.n_active = take(4);
+    p.bcount = take(2 * N * 4);
+    p.pairs = take(2 * N * S * 4);
     p.act = take(S * K * (size_t)c->F * dv.esz);
     p.yp = take(S * K * (size_t)c->d * 4);
     p.ws_total = o;
@@ -132,9 +128,10 @@ struct cmoe_handle {
     Layout lo;
     hipStream_t main = nullptr, side = nullptr;
     bool side_is_main = true;
-    std::vector<hipEvent_t> ev_access, ev_demand, ev_pro;
-    hipEvent_t ev_refine0 = nullptr;
-    int32_t t = 0;
+    std::vector<hipEvent_t> ev_access, ev_pro;
+    int32_t t = 0;            // next token
+    int64_t g = 0;            // layer steps accessed so far (bucket buffer parity)
+    std::vector<int> ver;     // current slot-map version of each layer
     int32_t R = 0;
     bool broken = false;
     // profiling
@@ -152,9 +149,9 @@ cmoe_status hip_fail(cmoe_handle* hd, hipError_t e, const char* where) {
     return fail(CMOE_ERR_HIP, std::string("HIP error in ") + where + ": " + hipGetErrorString(e));
 }
 
-#define HIPCHK(expr, where)                               \
-    do {                                                  \
-        hipError_t _e = (expr);                           \
+#define HIPCHK(expr, where)                                   \
+    do {                                                      \
+        hipError_t _e = (expr);                               \
         if (_e != hipSuccess) return hip_fail(hd, _e, where); \
     } while (0)
 
@@ -188,6 +185,14 @@ hipError_t timed(cmoe_handle* hd, int kid, hipStream_t st, F&& launch) {
     return e;
 }
 
+// One residency event of `layer` on stream st; advances the layer's slot-map
+// version.
+hipError_t fill(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, hipStream_t st) {
+    FillArgs f{layer, kind, hd->ver[layer], counted ? 1 : 0, zero_pre ? 1 : 0};
+    hd->ver[layer] ^= 1;
+    return timed(hd, KID_FILL, st, [&] { return cmoe::launch_fill(hd->lo, f, st); });
+}
+
 // One decode token.  h == nullptr selects injected logits (no router, no FFN).
 cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR, const float* zT, const float* zS) {
     const cmoe_config& c = hd->cfg;
@@ -195,50 +200,49 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
     const bool inject = h == nullptr;
     const bool full = c.mode == CMOE_MODE_SPATIO_TEMPORAL;
     const bool refine_on = full && hd->t >= 1 && hd->R > 0;
-    const uint32_t count = hd->t >= c.warmup_tokens ? cmoe::kFlagCount : 0u;
+    const bool counted = hd->t >= c.warmup_tokens;
+    const uint32_t count = counted ? cmoe::kFlagCount : 0u;
     hipStream_t M = hd->main, Sd = hd->side;
 
     if (refine_on) {  // layer 0: refined from the previous token's last-layer prediction
-        StepArgs a{0, 0, hd->R, cmoe::kFlagRefine | count, zR, zT, zS};
+        StepArgs a{0, 0, hd->R, 0, cmoe::kFlagRefine | count, zR, zT, zS};
         HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "refine layer 0");
-        HIPCHK(timed(hd, KID_FINISH, M, [&] { return cmoe::launch_finish(lo, a, M); }), "residency");
-        if (hd->side_is_main) {
-            HIPCHK(timed(hd, KID_FILL, M, [&] { return cmoe::launch_fill(lo, 0, 1, M); }), "fill");
-        } else {
-            HIPCHK(hipEventRecord(hd->ev_refine0, M), "event record");
-            HIPCHK(hipStreamWaitEvent(Sd, hd->ev_refine0, 0), "stream wait");
-            HIPCHK(timed(hd, KID_FILL, Sd, [&] { return cmoe::launch_fill(lo, 0, 1, Sd); }), "fill");
-            HIPCHK(hipEventRecord(hd->ev_pro[0], Sd), "event record");
+        if (!hd->side_is_main) {
+            HIPCHK(hipEventRecord(hd->ev_access[0], M), "event record");
+            HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[0], 0), "stream wait");
         }
+        HIPCHK(fill(hd, 0, 1, counted, false, Sd), "fill");
+        if (!hd->side_is_main) HIPCHK(hipEventRecord(hd->ev_pro[0], Sd), "event record");
     }
     for (int l = 0; l < c.L; ++l) {
         if (!inject) HIPCHK(timed(hd, KID_ROUTER, M, [&] { return cmoe::launch_router(lo, l, h, M); }), "router");
+        // the proactive fill of this layer reads its refined caches: it must end
+        // before the access below changes them
         if (refine_on && !hd->side_is_main) HIPCHK(hipStreamWaitEvent(M, hd->ev_pro[l], 0), "stream wait");
         const bool refine_next = refine_on && l + 1 < c.L;
         uint32_t flags = cmoe::kFlagAccess | count;
         if (inject) flags |= cmoe::kFlagInject;
         if (refine_on) flags |= cmoe::kFlagRefinedHere;
         if (refine_next) flags |= cmoe::kFlagRefine;
-        StepArgs a{l, l + 1, hd->R, flags, zR, zT, zS};
+        const int bbuf = (int)(hd->g & 1);
+        StepArgs a{l, l + 1, hd->R, bbuf, flags, zR, zT, zS};
         HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "cache step");
-        HIPCHK(timed(hd, KID_FINISH, M, [&] { return cmoe::launch_finish(lo, a, M); }), "residency");
-        if (hd->side_is_main) {
-            HIPCHK(timed(hd, KID_FILL, M, [&] { return cmoe::launch_fill(lo, l, 0, M); }), "fill");
-            if (refine_next) HIPCHK(timed(hd, KID_FILL, M, [&] { return cmoe::launch_fill(lo, l + 1, 1, M); }), "fill");
-        } else {
-            HIPCHK(hipEventRecord(hd->ev_access[l], M), "event record");
-            HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[l], 0), "stream wait");
-            HIPCHK(timed(hd, KID_FILL, Sd, [&] { return cmoe::launch_fill(lo, l, 0, Sd); }), "fill");
-            HIPCHK(hipEventRecord(hd->ev_demand[l], Sd), "event record");
-            if (refine_next) {
-                HIPCHK(timed(hd, KID_FILL, Sd, [&] { return cmoe::launch_fill(lo, l + 1, 1, Sd); }), "fill");
+        hd->g += 1;
+        HIPCHK(fill(hd, l, 0, counted, !refine_on, M), "fill");  // demand loads gate this layer's FFN
+        if (refine_next) {
+            if (hd->side_is_main) {
+                HIPCHK(fill(hd, l + 1, 1, counted, false, M), "fill");
+            } else {
+                HIPCHK(hipEventRecord(hd->ev_access[l], M), "event record");
+                HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[l], 0), "stream wait");
+                HIPCHK(fill(hd, l + 1, 1, counted, false, Sd), "fill");
                 HIPCHK(hipEventRecord(hd->ev_pro[l + 1], Sd), "event record");
             }
-            HIPCHK(hipStreamWaitEvent(M, hd->ev_demand[l], 0), "stream wait");
         }
         if (!inject) {
-            HIPCHK(timed(hd, KID_UP, M, [&] { return cmoe::launch_ffn_up(lo, l, h, M); }), "ffn up");
-            HIPCHK(timed(hd, KID_DOWN, M, [&] { return cmoe::launch_ffn_down(lo, l, M); }), "ffn down");
+            const int sv = hd->ver[l];
+            HIPCHK(timed(hd, KID_UP, M, [&] { return cmoe::launch_ffn_up(lo, l, bbuf, sv, h, M); }), "ffn up");
+            HIPCHK(timed(hd, KID_DOWN, M, [&] { return cmoe::launch_ffn_down(lo, l, bbuf, sv, M); }), "ffn down");
             HIPCHK(timed(hd, KID_COMBINE, M, [&] { return cmoe::launch_combine(lo, l, y, M); }), "combine");
         }
     }
@@ -290,10 +294,10 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     hd->dv = dv;
     hd->plan = make_plan(cfg, dv);
     hd->R = cfg->mode == CMOE_MODE_SPATIO_TEMPORAL ? cfg->R : 0;
+    hd->ver.assign(cfg->L, 0);
     hd->main = static_cast<hipStream_t>(main_stream);
-    hd->side = side_stream ? static_cast<hipStream_t>(side_stream) : hd->main;
     hd->side_is_main = side_stream == nullptr || side_stream == main_stream || (cfg->flags & CMOE_FLAG_FILL_ON_MAIN);
-    if (hd->side_is_main) hd->side = hd->main;
+    hd->side = hd->side_is_main ? hd->main : static_cast<hipStream_t>(side_stream);
 
     Layout& lo = hd->lo;
     const Plan& p = hd->plan;
@@ -310,36 +314,26 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.pS = reinterpret_cast<float*>(sb + p.pS);
     lo.ctr = reinterpret_cast<int64_t*>(sb + p.ctr);
     lo.phys = reinterpret_cast<int64_t*>(sb + p.phys);
-    lo.active_sum = reinterpret_cast<int64_t*>(sb + p.active_sum);
+    lo.active_sum = reinterpret_cast<unsigned long long*>(sb + p.active_sum);
     lo.slot_of = reinterpret_cast<int32_t*>(sb + p.slot_of);
     lo.slot_exp = reinterpret_cast<int32_t*>(sb + p.slot_exp);
-    lo.tile_count = reinterpret_cast<uint32_t*>(sb + p.tile_count);
-    lo.n_tiles = dv.tiles;
     lo.zpart = reinterpret_cast<double*>(wb + p.zpart);
     lo.logits = reinterpret_cast<float*>(wb + p.logits);
     lo.sel = reinterpret_cast<int32_t*>(wb + p.sel);
     lo.gates = reinterpret_cast<float*>(wb + p.gates);
     lo.events = reinterpret_cast<int32_t*>(wb + p.events);
     lo.step_fills = reinterpret_cast<int32_t*>(wb + p.step_fills);
-    lo.fill_list = reinterpret_cast<int32_t*>(wb + p.fill_list);
-    lo.fill_count = reinterpret_cast<int32_t*>(wb + p.fill_count);
-    lo.sel_mask = reinterpret_cast<unsigned long long*>(wb + p.sel_mask);
     lo.bcount = reinterpret_cast<int32_t*>(wb + p.bcount);
-    lo.boffset = reinterpret_cast<int32_t*>(wb + p.boffset);
     lo.pairs = reinterpret_cast<int32_t*>(wb + p.pairs);
-    lo.active = reinterpret_cast<int32_t*>(wb + p.active);
-    lo.n_active = reinterpret_cast<int32_t*>(wb + p.n_active);
     lo.act = wb + p.act;
     lo.yp = reinterpret_cast<float*>(wb + p.yp);
 
     auto mk = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
     hd->ev_access.resize(cfg->L);
-    hd->ev_demand.resize(cfg->L);
     hd->ev_pro.resize(cfg->L);
-    hipError_t e = mk(&hd->ev_refine0);
+    hipError_t e = hipSuccess;
     for (int l = 0; l < cfg->L && e == hipSuccess; ++l) {
         e = mk(&hd->ev_access[l]);
-        if (e == hipSuccess) e = mk(&hd->ev_demand[l]);
         if (e == hipSuccess) e = mk(&hd->ev_pro[l]);
     }
     if (e == hipSuccess) e = cmoe::launch_init(lo, hd->main);
@@ -457,6 +451,8 @@ cmoe_status cmoe_reset(cmoe_handle* hd) {
     HIPCHK(cmoe::launch_init(hd->lo, hd->main), "reset");
     HIPCHK(hipStreamSynchronize(hd->main), "reset");
     hd->t = 0;
+    hd->g = 0;
+    hd->ver.assign(hd->cfg.L, 0);
     return CMOE_OK;
 }
 
@@ -469,9 +465,7 @@ cmoe_status cmoe_destroy(cmoe_handle* hd) {
     auto rm = [](hipEvent_t e) {
         if (e) (void)hipEventDestroy(e);
     };
-    rm(hd->ev_refine0);
     for (auto e : hd->ev_access) rm(e);
-    for (auto e : hd->ev_demand) rm(e);
     for (auto e : hd->ev_pro) rm(e);
     for (auto e : hd->prof_pool) rm(e);
     delete hd;
@@ -502,8 +496,18 @@ cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t byte
     const size_t need = cmoe_view_bytes(hd, view);
     if (need == 0) return fail(CMOE_ERR_INVALID_ARG, "unknown view");
     if (!host_out || bytes < need) return fail(CMOE_ERR_INVALID_ARG, "output buffer too small");
-    const void* src = nullptr;
     const Layout& lo = hd->lo;
+    st = sync_all(hd);
+    if (st != CMOE_OK) return st;
+    if (view == CMOE_VIEW_SLOTS) {  // the current version of each layer's slot map
+        const size_t N = hd->cfg.N;
+        for (int l = 0; l < hd->cfg.L; ++l)
+            HIPCHK(hipMemcpy(static_cast<char*>(host_out) + l * N * 4,
+                             lo.slot_of + ((size_t)hd->ver[l] * hd->cfg.L + l) * N, N * 4, hipMemcpyDeviceToHost),
+                   "view read");
+        return CMOE_OK;
+    }
+    const void* src = nullptr;
     switch (view) {
         case CMOE_VIEW_LOGITS: src = lo.logits; break;
         case CMOE_VIEW_SELECTED: src = lo.sel; break;
@@ -511,13 +515,10 @@ cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t byte
         case CMOE_VIEW_CACHE: src = lo.cache; break;
         case CMOE_VIEW_COUNTERS: src = lo.ctr; break;
         case CMOE_VIEW_PHYS: src = lo.phys; break;
-        case CMOE_VIEW_SLOTS: src = lo.slot_of; break;
         case CMOE_VIEW_EVENTS: src = lo.events; break;
         case CMOE_VIEW_FILLS: src = lo.step_fills; break;
         case CMOE_VIEW_ACTIVE: src = lo.active_sum; break;
     }
-    st = sync_all(hd);
-    if (st != CMOE_OK) return st;
     HIPCHK(hipMemcpy(host_out, src, need, hipMemcpyDeviceToHost), "view read");
     return CMOE_OK;
 }

@@ -10,10 +10,12 @@
 // per 32 rows of W_down (down kernel), on the bf16 matrix core
 // (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  The expert's tokens form the
 // 16 columns of the B operand (groups of 16 tokens; several groups reuse the
-// loaded weights).  Each lane reads 32 consecutive bytes of its row per
-// 64-wide k chunk, the four lane groups of a row together one 128-byte line;
-// the two MFMAs of a chunk take k-slots kc + 16 g + {0..7} and
-// kc + 16 g + {8..15} for lane group g, the same for both operands.  The
+// loaded weights).  Per 64-wide k chunk, lane (r, g) of the A operand holds
+// W[row r][kc + 16 g .. + 16]; the two MFMAs of a chunk take k-slots
+// kc + 16 g + {0..7} and kc + 16 g + {8..15}, the same for both operands.
+// The weights come from the expert's HBM slot in packed order (the fill
+// kernel writes it so): each A operand load of a wavefront reads one
+// contiguous kilobyte and each wavefront streams one contiguous block.  The
 // SwiGLU intermediate is stored in bf16 (the input type of the down kernel's
 // matrix core).
 //
@@ -50,29 +52,28 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
     return (a >> 16) | (b & 0xFFFF0000u);
 }
 
-// Weights of expert e of layer l in its HBM slot, or nullptr if it has none
-// (cannot happen for a selected expert: the residency step maps every member
-// of any cache, and selected experts are members).
-__device__ inline const uint16_t* expert_base(const Layout& lo, int l, int e) {
-    const int slot = lo.slot_of[(int64_t)l * lo.N + e];
+// Weights of expert e of layer l in its HBM slot (slot map version sv), or
+// nullptr if it has none (cannot happen for a selected expert: the residency
+// step maps every member of any cache, and selected experts are members).
+__device__ inline const uint16_t* expert_base(const Layout& lo, int l, int sv, int e) {
+    const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
     if (slot < 0 || slot >= lo.n_slots) return nullptr;
     return reinterpret_cast<const uint16_t*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems;
 }
 
 // ---------------------------------------------------------------- bf16
-__global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, const uint16_t* __restrict__ h) {
+__global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, int bbuf, int sv, const uint16_t* __restrict__ h) {
     const int ftn = lo.F / 16;
-    const int a = blockIdx.x / ftn, ft = blockIdx.x - a * ftn;
-    if (a >= *lo.n_active) return;
-    const int e = lo.active[a];
-    const int m = lo.bcount[e], off = lo.boffset[e];
-    const uint16_t* Wg = expert_base(lo, l, e);
+    const int e = blockIdx.x / ftn, ft = blockIdx.x - e * ftn;
+    const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
+    if (m == 0) return;
+    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
+    const uint16_t* Wg = expert_base(lo, l, sv, e);
     if (!Wg) return;
-    const uint16_t* Wu = Wg + (int64_t)lo.F * lo.d;
     const int lane = threadIdx.x, r = lane & 15, g = lane >> 4;
-    const int64_t arow = (int64_t)(ft * 16 + r) * lo.d + 16 * g;
-    const uint16_t* ag = Wg + arow;
-    const uint16_t* au = Wu + arow;
+    // packed slot layout: chunk c of this row tile is 256 units of 16 bytes,
+    // gate half 0, gate half 1, up half 0, up half 1, each 64 units
+    const uint4* tileA = reinterpret_cast<const uint4*>(Wg) + (int64_t)ft * (lo.d / 64) * 256 + lane;
     uint16_t* act = reinterpret_cast<uint16_t*>(lo.act);
     const int d = lo.d;
     const int nchunk = d / 64;
@@ -85,7 +86,7 @@ __global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, const uint16
         for (int q = 0; q < kNG; ++q) {
             const int tok = t0 + 16 * q + r;
             xv[q] = q < ng && tok < m;
-            const int s = xv[q] ? (lo.pairs[off + tok] >> 8) : 0;
+            const int s = xv[q] ? (bk[tok] >> 8) : 0;
             xb[q] = h + ((int64_t)s * lo.L + l) * d + 16 * g;
         }
         f32x4 cg[kNG], cu[kNG];
@@ -99,11 +100,11 @@ __global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, const uint16
             uint4 G[kUnroll][2], U[kUnroll][2];
 #pragma unroll
             for (int i = 0; i < kUnroll; ++i) {
-                const int kc = (c + i) * 64;
-                G[i][0] = *reinterpret_cast<const uint4*>(ag + kc);
-                G[i][1] = *reinterpret_cast<const uint4*>(ag + kc + 8);
-                U[i][0] = *reinterpret_cast<const uint4*>(au + kc);
-                U[i][1] = *reinterpret_cast<const uint4*>(au + kc + 8);
+                const uint4* ch = tileA + (int64_t)(c + i) * 256;
+                G[i][0] = ch[0];
+                G[i][1] = ch[64];
+                U[i][0] = ch[128];
+                U[i][1] = ch[192];
             }
 #pragma unroll
             for (int q = 0; q < kNG; ++q) {
@@ -125,10 +126,11 @@ __global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, const uint16
         }
         for (; c < nchunk; ++c) {
             const int kc = c * 64;
-            const uint4 g0 = *reinterpret_cast<const uint4*>(ag + kc);
-            const uint4 g1 = *reinterpret_cast<const uint4*>(ag + kc + 8);
-            const uint4 u0 = *reinterpret_cast<const uint4*>(au + kc);
-            const uint4 u1 = *reinterpret_cast<const uint4*>(au + kc + 8);
+            const uint4* ch = tileA + (int64_t)c * 256;
+            const uint4 g0 = ch[0];
+            const uint4 g1 = ch[64];
+            const uint4 u0 = ch[128];
+            const uint4 u1 = ch[192];
 #pragma unroll
             for (int q = 0; q < kNG; ++q) {
                 if (q >= ng) break;
@@ -152,25 +154,29 @@ __global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, const uint16
                 uint2 o;
                 o.x = pack_bf16x2(silu_mul(cg[q][0], cu[q][0]), silu_mul(cg[q][1], cu[q][1]));
                 o.y = pack_bf16x2(silu_mul(cg[q][2], cu[q][2]), silu_mul(cg[q][3], cu[q][3]));
-                *reinterpret_cast<uint2*>(act + (int64_t)(off + tok) * lo.F + ft * 16 + 4 * g) = o;
+                const int pair = bk[tok];
+                const int64_t row = (int64_t)(pair >> 8) * lo.K + (pair & 255);  // token (s, k)
+                *reinterpret_cast<uint2*>(act + row * lo.F + ft * 16 + 4 * g) = o;
             }
         }
     }
 }
 
-__global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l) {
+__global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l, int bbuf, int sv) {
     const int dtn = lo.d / 32;
-    const int a = blockIdx.x / dtn, dt = blockIdx.x - a * dtn;
-    if (a >= *lo.n_active) return;
-    const int e = lo.active[a];
-    const int m = lo.bcount[e], off = lo.boffset[e];
+    const int e = blockIdx.x / dtn, dt = blockIdx.x - e * dtn;
+    const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
+    if (m == 0) return;
+    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
     const int F = lo.F;
-    const uint16_t* Wbase = expert_base(lo, l, e);
+    const uint16_t* Wbase = expert_base(lo, l, sv, e);
     if (!Wbase) return;
-    const uint16_t* Wd = Wbase + 2 * (int64_t)F * lo.d;
     const int lane = threadIdx.x, r = lane & 15, g = lane >> 4;
-    const uint16_t* a0 = Wd + (int64_t)(dt * 32 + r) * F + 16 * g;
-    const uint16_t* a1 = a0 + 16 * (int64_t)F;
+    // packed slot layout: after the gate/up part (F d / 4 units), chunk c of
+    // this 32-row tile is 256 units: rows 0-15 half 0, half 1, rows 16-31
+    // half 0, half 1, each 64 units
+    const uint4* tileB =
+        reinterpret_cast<const uint4*>(Wbase) + (int64_t)F * lo.d / 4 + (int64_t)dt * (F / 64) * 256 + lane;
     const uint16_t* act = reinterpret_cast<const uint16_t*>(lo.act);
     const int nchunk = F / 64;
 
@@ -182,7 +188,8 @@ __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l) {
         for (int q = 0; q < kNG; ++q) {
             const int tok = t0 + 16 * q + r;
             xv[q] = q < ng && tok < m;
-            xb[q] = act + (int64_t)(off + (xv[q] ? tok : 0)) * F + 16 * g;
+            const int pair = xv[q] ? bk[tok] : 0;
+            xb[q] = act + ((int64_t)(pair >> 8) * lo.K + (pair & 255)) * F + 16 * g;
         }
         f32x4 c0[kNG], c1[kNG];
 #pragma unroll
@@ -195,11 +202,11 @@ __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l) {
             uint4 A0[kUnroll][2], A1[kUnroll][2];
 #pragma unroll
             for (int i = 0; i < kUnroll; ++i) {
-                const int kc = (c + i) * 64;
-                A0[i][0] = *reinterpret_cast<const uint4*>(a0 + kc);
-                A0[i][1] = *reinterpret_cast<const uint4*>(a0 + kc + 8);
-                A1[i][0] = *reinterpret_cast<const uint4*>(a1 + kc);
-                A1[i][1] = *reinterpret_cast<const uint4*>(a1 + kc + 8);
+                const uint4* ch = tileB + (int64_t)(c + i) * 256;
+                A0[i][0] = ch[0];
+                A0[i][1] = ch[64];
+                A1[i][0] = ch[128];
+                A1[i][1] = ch[192];
             }
 #pragma unroll
             for (int q = 0; q < kNG; ++q) {
@@ -221,10 +228,11 @@ __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l) {
         }
         for (; c < nchunk; ++c) {
             const int kc = c * 64;
-            const uint4 p0 = *reinterpret_cast<const uint4*>(a0 + kc);
-            const uint4 p1 = *reinterpret_cast<const uint4*>(a0 + kc + 8);
-            const uint4 q0 = *reinterpret_cast<const uint4*>(a1 + kc);
-            const uint4 q1 = *reinterpret_cast<const uint4*>(a1 + kc + 8);
+            const uint4* ch = tileB + (int64_t)c * 256;
+            const uint4 p0 = ch[0];
+            const uint4 p1 = ch[64];
+            const uint4 q0 = ch[128];
+            const uint4 q1 = ch[192];
 #pragma unroll
             for (int q = 0; q < kNG; ++q) {
                 if (q >= ng) break;
@@ -244,7 +252,7 @@ __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l) {
             if (q >= ng) break;
             const int tok = t0 + 16 * q + r;
             if (tok < m) {
-                const int pair = lo.pairs[off + tok];
+                const int pair = bk[tok];
                 const int s = pair >> 8, k = pair & 255;
                 const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
                 float* dst = lo.yp + ((int64_t)s * lo.K + k) * lo.d + dt * 32 + 4 * g;
@@ -257,46 +265,47 @@ __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l) {
 }
 
 // ---------------------------------------------------------------- fp32
-__global__ __launch_bounds__(64) void ffn_up_f32(Layout lo, int l, const float* __restrict__ h) {
+__global__ __launch_bounds__(64) void ffn_up_f32(Layout lo, int l, int bbuf, int sv, const float* __restrict__ h) {
     const int ftn = lo.F / 64;
-    const int a = blockIdx.x / ftn, ft = blockIdx.x - a * ftn;
-    if (a >= *lo.n_active) return;
-    const int e = lo.active[a];
-    const int m = lo.bcount[e], off = lo.boffset[e];
-    const int slot = lo.slot_of[(int64_t)l * lo.N + e];
+    const int e = blockIdx.x / ftn, ft = blockIdx.x - e * ftn;
+    const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
+    if (m == 0) return;
+    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
+    const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
     if (slot < 0 || slot >= lo.n_slots) return;
     const float* Wg = reinterpret_cast<const float*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems;
     const float* Wu = Wg + (int64_t)lo.F * lo.d;
     const int f = ft * 64 + threadIdx.x;
     float* act = reinterpret_cast<float*>(lo.act);
     for (int tok = 0; tok < m; ++tok) {
-        const int s = lo.pairs[off + tok] >> 8;
+        const int pair = bk[tok];
+        const int s = pair >> 8;
         const float* x = h + ((int64_t)s * lo.L + l) * lo.d;
         float ag = 0.0f, au = 0.0f;
         for (int i = 0; i < lo.d; ++i) {
             ag = __builtin_fmaf(Wg[(int64_t)f * lo.d + i], x[i], ag);
             au = __builtin_fmaf(Wu[(int64_t)f * lo.d + i], x[i], au);
         }
-        act[(int64_t)(off + tok) * lo.F + f] = ag / (1.0f + expf(-ag)) * au;
+        act[((int64_t)s * lo.K + (pair & 255)) * lo.F + f] = ag / (1.0f + expf(-ag)) * au;
     }
 }
 
-__global__ __launch_bounds__(64) void ffn_down_f32(Layout lo, int l) {
+__global__ __launch_bounds__(64) void ffn_down_f32(Layout lo, int l, int bbuf, int sv) {
     const int dtn = lo.d / 64;
-    const int a = blockIdx.x / dtn, dt = blockIdx.x - a * dtn;
-    if (a >= *lo.n_active) return;
-    const int e = lo.active[a];
-    const int m = lo.bcount[e], off = lo.boffset[e];
-    const int slot = lo.slot_of[(int64_t)l * lo.N + e];
+    const int e = blockIdx.x / dtn, dt = blockIdx.x - e * dtn;
+    const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
+    if (m == 0) return;
+    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
+    const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
     if (slot < 0 || slot >= lo.n_slots) return;
     const float* Wd = reinterpret_cast<const float*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems +
                       2 * (int64_t)lo.F * lo.d;
     const int j = dt * 64 + threadIdx.x;
     const float* act = reinterpret_cast<const float*>(lo.act);
     for (int tok = 0; tok < m; ++tok) {
-        const int pair = lo.pairs[off + tok];
+        const int pair = bk[tok];
         const int s = pair >> 8, k = pair & 255;
-        const float* av = act + (int64_t)(off + tok) * lo.F;
+        const float* av = act + ((int64_t)s * lo.K + k) * lo.F;
         float acc = 0.0f;
         for (int f = 0; f < lo.F; ++f) acc = __builtin_fmaf(Wd[(int64_t)j * lo.F + f], av[f], acc);
         const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
@@ -337,23 +346,21 @@ __global__ __launch_bounds__(64) void combine_kernel(Layout lo, int l, float* __
 
 }  // namespace
 
-hipError_t launch_ffn_up(const Layout& lo, int l, const void* h, hipStream_t st) {
-    const int max_active = lo.N < lo.S * lo.K ? lo.N : lo.S * lo.K;
+hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st) {
     if (lo.dtype == 1)
-        hipLaunchKernelGGL(ffn_up_bf16, dim3(max_active * (lo.F / 16)), dim3(64), 0, st, lo, l,
+        hipLaunchKernelGGL(ffn_up_bf16, dim3(lo.N * (lo.F / 16)), dim3(64), 0, st, lo, l, bbuf, sv,
                            static_cast<const uint16_t*>(h));
     else
-        hipLaunchKernelGGL(ffn_up_f32, dim3(max_active * (lo.F / 64)), dim3(64), 0, st, lo, l,
+        hipLaunchKernelGGL(ffn_up_f32, dim3(lo.N * (lo.F / 64)), dim3(64), 0, st, lo, l, bbuf, sv,
                            static_cast<const float*>(h));
     return hipGetLastError();
 }
 
-hipError_t launch_ffn_down(const Layout& lo, int l, hipStream_t st) {
-    const int max_active = lo.N < lo.S * lo.K ? lo.N : lo.S * lo.K;
+hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st) {
     if (lo.dtype == 1)
-        hipLaunchKernelGGL(ffn_down_bf16, dim3(max_active * (lo.d / 32)), dim3(64), 0, st, lo, l);
+        hipLaunchKernelGGL(ffn_down_bf16, dim3(lo.N * (lo.d / 32)), dim3(64), 0, st, lo, l, bbuf, sv);
     else
-        hipLaunchKernelGGL(ffn_down_f32, dim3(max_active * (lo.d / 64)), dim3(64), 0, st, lo, l);
+        hipLaunchKernelGGL(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), 0, st, lo, l, bbuf, sv);
     return hipGetLastError();
 }
 

@@ -1,37 +1,168 @@
-// fill.hip - copies newly resident experts from the cold pool into their HBM
-// slots (the demand loads and proactive loads of Section 2 / Algorithm 2, as
-// physical transfers).  The list of (expert, slot) pairs and its length are
-// produced on the device by the residency step, so the copy is a kernel that
-// reads the list rather than host-issued memcpys: no host synchronisation per
-// layer.  With an empty list it returns at once.  The pool may be pinned host
-// memory mapped into the device; the copy then runs over the host link.
+// fill.hip - physical residency and expert copies (the demand loads and
+// proactive loads of Section 2 / Algorithm 2 as transfers into HBM slots).
+//
+// One launch handles one residency event of one layer: after the post-access
+// update (demand loads) or after refinement (proactive loads), the layer's
+// HBM slots must hold the union U of the streams' caches.  Experts that left
+// U free their slot; each new expert, in ascending order, takes the lowest
+// free slot and is copied there from the cold pool.
+//
+// Every workgroup derives the same assignment from the same inputs (the
+// caches and the slot maps of version rv, which nobody writes during the
+// launch), then copies its share of the new experts; workgroup 0 also writes
+// the new slot maps (version rv ^ 1).  No workgroup waits for another, and
+// the host never has to read the fill list.  The pool may be pinned host
+// memory mapped into the device; copies then run over the host link.
 #include "cmoe_internal.h"
 
 namespace cmoe {
 
 namespace {
 
-__global__ __launch_bounds__(256) void fill_kernel(Layout lo, int l, int kind) {
-    const int n = lo.fill_count[l * 2 + kind];
-    if (n == 0) return;
+// Exclusive prefix sum over the 256 threads of the block; *total gets the sum.
+__device__ int block_scan(int v, int* total, int* lds4) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) lds4[w] = x;
+    __syncthreads();
+    int off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if (i < w) off += lds4[i];
+        tot += lds4[i];
+    }
+    __syncthreads();
+    *total = tot;
+    return off + x - v;
+}
+
+// bf16 experts are stored in their HBM slot in the order the FFN kernels
+// consume them, so that every load instruction reads 1 KB of contiguous
+// memory.  Units are 16 bytes (8 bf16); lane l of a wavefront takes unit l of
+// a 64-unit run.
+//   gate/up part, units [0, F d / 4):
+//     ((((ft * (d/64) + c) * 2 + mat) * 2 + half) * 64 + lane)
+//     = W_mat[16 ft + lane % 16][64 c + 16 (lane / 16) + 8 half .. + 8],
+//     mat 0 = gate, 1 = up
+//   down part, units [F d / 4, 3 F d / 8):
+//     F d / 4 + ((((dt * (F/64) + c) * 2 + mt) * 2 + half) * 64 + lane)
+//     = W_down[32 dt + 16 mt + lane % 16][64 c + 16 (lane / 16) + 8 half .. + 8]
+// The cold pool keeps the plain row-major layout; this maps a slot unit to
+// its pool unit.
+__device__ inline int64_t packed_source_unit(int u, int d, int F) {
+    const int partA = F / 16 * (d / 64) * 256;
+    int lane, half, sub, c, tile, row, col, rows_per_tile, ncol_chunks;
+    int64_t base;
+    if (u < partA) {
+        ncol_chunks = d / 64;
+        rows_per_tile = 16;
+        lane = u & 63;
+        int t = u >> 6;
+        half = t & 1;
+        t >>= 1;
+        sub = t & 1;  // gate or up
+        t >>= 1;
+        c = t % ncol_chunks;
+        tile = t / ncol_chunks;
+        row = rows_per_tile * tile + (lane & 15);
+        col = 64 * c + 16 * (lane >> 4) + 8 * half;
+        base = (int64_t)sub * F * d + (int64_t)row * d + col;
+    } else {
+        const int v = u - partA;
+        ncol_chunks = F / 64;
+        lane = v & 63;
+        int t = v >> 6;
+        half = t & 1;
+        t >>= 1;
+        sub = t & 1;  // 16-row half of the 32-row tile
+        t >>= 1;
+        c = t % ncol_chunks;
+        tile = t / ncol_chunks;
+        row = 32 * tile + 16 * sub + (lane & 15);
+        col = 64 * c + 16 * (lane >> 4) + 8 * half;
+        base = 2 * (int64_t)F * d + (int64_t)row * F + col;
+    }
+    return base / 8;
+}
+
+__global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
+    __shared__ unsigned long long U[4];
+    __shared__ int so[kMaxN], se[kMaxN], free_list[kMaxN], enter_list[kMaxN], lds4[4];
+    const int tid = threadIdx.x;
+    const int N = lo.N, layer = f.layer;
+    const int32_t* so_in = lo.slot_of + ((int64_t)f.rv * lo.L + layer) * N;
+    const int32_t* se_in = lo.slot_exp + ((int64_t)f.rv * lo.L + layer) * lo.n_slots;
+    if (tid < 4) U[tid] = 0ull;
+    if (tid < N) so[tid] = so_in[tid];
+    if (tid < lo.n_slots) se[tid] = se_in[tid];
+    __syncthreads();
+    for (int i = tid; i < lo.S * lo.NW; i += blockDim.x) {
+        const int s = i / lo.NW, j = i - s * lo.NW;
+        const unsigned long long w = lo.cache[((int64_t)s * lo.L + layer) * lo.NW + j];
+        if (w) atomicOr(&U[j], w);
+    }
+    __syncthreads();
+    const int e = tid;
+    const bool inU = e < N && ((U[e >> 6] >> (e & 63)) & 1ull);
+    int cur = e < N ? so[e] : -1;
+    if (e < N && cur >= 0 && !inU) {  // left every cache: free its slot
+        se[cur] = -1;
+        so[e] = -1;
+        cur = -1;
+    }
+    __syncthreads();
+    const bool enter = e < N && inU && cur < 0;
+    const bool is_free = tid < lo.n_slots && se[tid] == -1;
+    int nfree, nenter;
+    const int rf = block_scan(is_free ? 1 : 0, &nfree, lds4);
+    if (is_free) free_list[rf] = tid;
+    const int re = block_scan(enter ? 1 : 0, &nenter, lds4);
+    __syncthreads();
+    if (enter) {  // rank re among new experts takes the rank-re free slot
+        const int q = free_list[re];
+        so[e] = q;
+        se[q] = e;
+        enter_list[re] = e;
+    }
+    __syncthreads();
+    if (blockIdx.x == 0) {
+        int32_t* so_out = lo.slot_of + ((int64_t)(f.rv ^ 1) * lo.L + layer) * N;
+        int32_t* se_out = lo.slot_exp + ((int64_t)(f.rv ^ 1) * lo.L + layer) * lo.n_slots;
+        if (tid < N) so_out[tid] = so[tid];
+        if (tid < lo.n_slots) se_out[tid] = se[tid];
+        if (tid == 0) {
+            lo.step_fills[layer * 2 + f.kind] = nenter;
+            if (f.zero_pre) lo.step_fills[layer * 2 + 1] = 0;
+            if (f.counted) lo.phys[layer * 2 + f.kind] += nenter;
+        }
+    }
+    if (nenter == 0) return;
     const int64_t bytes = lo.expert_elems * (lo.dtype == 1 ? 2 : 4);
     const int64_t n16 = bytes / 16;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tid;
     const int64_t gs = (int64_t)gridDim.x * blockDim.x;
-    const int32_t* fl = lo.fill_list + ((int64_t)l * 2 + kind) * lo.N * 2;
-    for (int f = 0; f < n; ++f) {
-        const int e = fl[2 * f], q = fl[2 * f + 1];
+    for (int k = 0; k < nenter; ++k) {
+        const int ex = enter_list[k], q = so[ex];
         const uint4* src =
-            reinterpret_cast<const uint4*>(static_cast<const char*>(lo.pool) + ((int64_t)l * lo.N + e) * bytes);
-        uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(lo.arena) + ((int64_t)l * lo.n_slots + q) * bytes);
-        for (int64_t i = gid; i < n16; i += gs) dst[i] = src[i];
+            reinterpret_cast<const uint4*>(static_cast<const char*>(lo.pool) + ((int64_t)layer * N + ex) * bytes);
+        uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(lo.arena) + ((int64_t)layer * lo.n_slots + q) * bytes);
+        if (lo.dtype == 1) {
+            for (int64_t i = gid; i < n16; i += gs) dst[i] = src[packed_source_unit((int)i, lo.d, lo.F)];
+        } else {
+            for (int64_t i = gid; i < n16; i += gs) dst[i] = src[i];
+        }
     }
 }
 
 }  // namespace
 
-hipError_t launch_fill(const Layout& lo, int l, int kind, hipStream_t st) {
-    hipLaunchKernelGGL(fill_kernel, dim3(512), dim3(256), 0, st, lo, l, kind);
+hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st) {
+    hipLaunchKernelGGL(fill_kernel, dim3(kFillBlocks), dim3(256), 0, st, lo, f);
     return hipGetLastError();
 }
 

@@ -140,3 +140,57 @@ def test_fills_copy_the_right_expert_bytes():
             if q >= 0:
                 assert torch.equal(arena[l, q], pool[l, e]), (l, e, q)
     eng.cmoe_destroy()
+
+
+def packed_from_plain(plain_u16, d, F):
+    """The packed slot order of a bf16 expert (see fill.hip), written out from
+    its documented formula: 16-byte units of 8 bf16."""
+    Wg = plain_u16[: F * d].reshape(F, d)
+    Wu = plain_u16[F * d: 2 * F * d].reshape(F, d)
+    Wd = plain_u16[2 * F * d:].reshape(d, F)
+    units = []
+    for ft in range(F // 16):
+        for c in range(d // 64):
+            for mat in (Wg, Wu):
+                for half in range(2):
+                    for lane in range(64):
+                        row, col = 16 * ft + lane % 16, 64 * c + 16 * (lane // 16) + 8 * half
+                        units.append(mat[row, col:col + 8])
+    for dt in range(d // 32):
+        for c in range(F // 64):
+            for mt in range(2):
+                for half in range(2):
+                    for lane in range(64):
+                        row, col = 32 * dt + 16 * mt + lane % 16, 64 * c + 16 * (lane // 16) + 8 * half
+                        units.append(Wd[row, col:col + 8])
+    return np.concatenate(units)
+
+
+def test_bf16_slots_hold_the_packed_expert():
+    from paper_2609_04895_amd import cmoe as B
+    L, N, K, C, S, d, F = 2, 8, 2, 3, 3, 128, 128
+    dev = torch.device("cuda", 0)
+    w = torch.zeros((L, N, d), dtype=torch.bfloat16, device=dev)
+    per = 3 * d * F
+    gen = torch.Generator().manual_seed(3)
+    pool_cpu = torch.randint(0, 2 ** 16, (L, N, per), generator=gen, dtype=torch.int32).to(torch.int16)
+    pool = pool_cpu.view(torch.bfloat16).to(dev)
+    cfg = B.make_config(L, N, K, d, F, C, 0, S, 0, B.CMOE_BF16)
+    eng = B.Engine(cfg, w, w, None, None, pool)
+    rng = np.random.default_rng(4)
+    z = logits_sequence(rng, 5, S, L, N, ties=False)
+    for t in range(5):
+        eng.cmoe_step_logits(torch.from_numpy(z[t, 0]).to(dev), torch.from_numpy(z[t, 1]).to(dev))
+    slots = eng.cmoe_read(B.CMOE_VIEW_SLOTS)
+    n_slots = min(N, S * C)
+    arena = eng.arena[: L * n_slots * per * 2].view(torch.int16).cpu().numpy().view(np.uint16).reshape(L, n_slots, per)
+    plain = pool_cpu.numpy().view(np.uint16)
+    checked = 0
+    for l in range(L):
+        for e in range(N):
+            q = int(slots[l, e])
+            if q >= 0:
+                assert np.array_equal(arena[l, q], packed_from_plain(plain[l, e], d, F)), (l, e, q)
+                checked += 1
+    assert checked > 0
+    eng.cmoe_destroy()
