@@ -24,6 +24,26 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "ffn_up_bf16_qwen3_30b_traffic.md")
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per ffn_up launch from the committed rocprofv3 counter runs,
+    or None if they were taken on another workload or on other kernel sources."""
+    import hashlib
+    if workload_name != "qwen3_30b" or not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_PROFILE):
+        if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "sources_sha256"):
+            k, v = line.split(":", 1)
+            vals[k] = v.strip()
+    src = os.path.join(ROOT, "paper_2609_04895_amd", "csrc")
+    digest = hashlib.sha256(open(os.path.join(src, "ffn.hip"), "rb").read()
+                            + open(os.path.join(src, "fill.hip"), "rb").read()).hexdigest()
+    if vals.get("sources_sha256") != digest:
+        return None
+    return float(vals["traffic_bytes_per_launch"])
 METRIC = "cache-aware MoE decode token-layer steps/s per GPU; % HBM roofline; hit rate"
 
 
@@ -90,6 +110,9 @@ def main():
     ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
     ap.add_argument("--no-profile", action="store_true", help="no per-kernel HIP events in the timed region")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after the timed region, run one elementwise device copy of 1 GiB (reference "
+                         "kernel for scaling rocprofv3 byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -179,7 +202,7 @@ def main():
         gbs = bytes_up / avg_s / 1e9
         res["roofline"] = {"kernel": "ffn_up_bf16" if w.dtype == 1 else "ffn_up_f32", "bound": "hbm",
                            "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
-                           "traffic": None, "avg_launch_us": avg_s * 1e6, "algorithmic_bytes_per_launch": bytes_up}
+                           "traffic": measured_traffic(w.name), "avg_launch_us": avg_s * 1e6, "algorithmic_bytes_per_launch": bytes_up}
 
     A, D, P, Tc = tot["accesses"], tot["demand_misses"], tot["proactive_loads"], tot["tokens"]
     res["cache"] = {"hit": 1 - D / A, "adj_hit": (A - D) / (A + P), "load_mb_per_token": (D + P) * w.expert_bytes
@@ -188,6 +211,12 @@ def main():
     print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
     eng.cmoe_destroy()
     del inputs, hidden
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")   # 1 GiB
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)   # one elementwise kernel: reads 1 GiB, writes 1 GiB
+        torch.cuda.synchronize()
+        del src, dst
     if args.cpu_seconds > 0:
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(res), flush=True)
