@@ -181,7 +181,7 @@ __device__ inline void clear_bit(unsigned long long (&w)[NPL], int e) {
 // Pre-access refinement of one (stream, layer) cache (Algorithm 2).
 template <int NPL>
 __device__ void refine_one(const Layout& lo, int s, int rl, int R, bool counted, const float (&pred)[NPL],
-                           const float (&aTv)[NPL], const unsigned long long (&cw_in)[NPL], int lane) {
+                           const float (&aTv)[NPL], const unsigned long long (&cw_in)[NPL], int64_t ctr_p, int lane) {
     const int N = lo.N;
     float sST[NPL];
     unsigned long long cand[NPL];
@@ -235,11 +235,11 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, bool counted,
     if (lane == 0) {
         for (int j = 0; j < lo.NW; ++j) cptr[j] = cw[j];
         lo.events[((int64_t)rl * lo.S + s) * 4 + 2] = nP;
-        if (counted) lo.ctr[((int64_t)s * lo.L + rl) * kNctr + kCtrP] += nP;
+        if (counted) lo.ctr[((int64_t)s * lo.L + rl) * kNctr + kCtrP] = ctr_p + nP;
     }
 }
 
-template <int NPL>
+template <int NPL, int NR, bool INJECT>
 __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane) {
     const int N = lo.N, L = lo.L, K = lo.K;
     const bool full = lo.mode == 1;
@@ -252,6 +252,15 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
     float aTv[NPL];
     unsigned long long cw_r[NPL], cw_a[NPL];
     const bool refine = (a.flags & kFlagRefine) != 0;
+    // counters this wavefront updates (lane 0 owns them)
+    int64_t ctr_a[kNctr] = {0, 0, 0, 0, 0}, ctr_rp = 0;
+    if (lane == 0 && counted) {
+        if (a.flags & kFlagAccess) {
+#pragma unroll
+            for (int c = 0; c < kNctr; ++c) ctr_a[c] = lo.ctr[((int64_t)s * L + a.l) * kNctr + c];
+        }
+        if (refine) ctr_rp = lo.ctr[((int64_t)s * L + a.rl) * kNctr + kCtrP];
+    }
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
         const int e = j * 64 + lane;
@@ -263,36 +272,52 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
     if (a.flags & kFlagAccess) {
         const int l = a.l;
         const int64_t sl = (int64_t)s * L + l;
-        // logits
+        // logits: every load is issued first (router split partials, padded to
+        // kMaxSplit per logit, or the injected logits; the native bias, a zero
+        // row when there is none), then the splits are added in ascending
+        // order and rounded once
+        const float* brow = lo.bias ? lo.bias + (int64_t)l * N : lo.zero_row;
+        double2 pv[NR][NPL][kMaxSplit / 2];
+        float zin[NR][NPL], bz[NPL];
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+            const int e = j * 64 + lane;
+            const int ec = e < N ? e : N - 1;  // lanes past N read a valid address and discard it
+            bz[j] = brow[ec];
+#pragma unroll
+            for (int r = 0; r < NR; ++r) {
+                if (INJECT) {
+                    const float* src = r == 0 ? a.zR : (r == 1 ? a.zT : a.zS);
+                    zin[r][j] = src[sl * N + ec];
+                } else {
+                    const double2* zp =
+                        reinterpret_cast<const double2*>(lo.zpart + (((int64_t)s * NR + r) * N + ec) * kMaxSplit);
+#pragma unroll
+                    for (int u = 0; u < kMaxSplit / 2; ++u) pv[r][j][u] = zp[u];
+                }
+            }
+        }
         float z[3][NPL];
 #pragma unroll
-        for (int r = 0; r < 3; ++r) {
+        for (int j = 0; j < NPL; ++j) z[2][j] = 0.0f;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
 #pragma unroll
             for (int j = 0; j < NPL; ++j) {
-                z[r][j] = 0.0f;
-                if (r >= lo.n_r) continue;
-                const int e = j * 64 + lane;
-                float v = 0.0f;
-                if (e < N) {
-                    if (a.flags & kFlagInject) {
-                        const float* src = r == 0 ? a.zR : (r == 1 ? a.zT : a.zS);
-                        v = src[sl * N + e];
-                    } else {
-                        // router splits of this logit, added in ascending split order
-                        const double* zp = lo.zpart + (((int64_t)s * lo.n_r + r) * N + e) * lo.nsplit;
-                        double pv[kMaxSplit];
+                float v;
+                if (INJECT) {
+                    v = zin[r][j];
+                } else {
+                    double acc = 0.0;
 #pragma unroll
-                        for (int p = 0; p < kMaxSplit; ++p) pv[p] = p < lo.nsplit ? zp[p] : 0.0;
-                        double acc = 0.0;
-#pragma unroll
-                        for (int p = 0; p < kMaxSplit; ++p)
-                            if (p < lo.nsplit) acc += pv[p];
-                        if (r == 0 && lo.bias) acc += (double)lo.bias[(int64_t)l * N + e];
-                        v = (float)acc;
-                    }
-                    lo.logits[(((int64_t)l * lo.S + s) * lo.n_r + r) * N + e] = v;
+                    for (int p = 0; p < kMaxSplit; ++p)
+                        if (p < lo.nsplit) acc += (p & 1) ? pv[r][j][p >> 1].y : pv[r][j][p >> 1].x;
+                    if (r == 0) acc += (double)bz[j];
+                    v = (float)acc;
                 }
-                z[r][j] = v;
+                const int e = j * 64 + lane;
+                if (e < N) lo.logits[(((int64_t)l * lo.S + s) * NR + r) * N + e] = v;
+                z[r][j] = e < N ? v : 0.0f;
             }
         }
         float pR[NPL], pT[NPL];
@@ -391,10 +416,10 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             ev[3] = 0;
             if (counted) {
                 int64_t* c = lo.ctr + sl * kNctr;
-                c[kCtrA] += K;
-                c[kCtrHits] += hits;
-                c[kCtrD] += nD;
-                c[kCtrT] += 1;
+                c[kCtrA] = ctr_a[kCtrA] + K;
+                c[kCtrHits] = ctr_a[kCtrHits] + hits;
+                c[kCtrD] = ctr_a[kCtrD] + nD;
+                c[kCtrT] = ctr_a[kCtrT] + 1;
             }
         }
         if (full) {
@@ -415,10 +440,10 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             pred[j] = e < N ? lo.pS[(int64_t)s * N + e] : 0.0f;
         }
     }
-    if (refine) refine_one<NPL>(lo, s, a.rl, a.R, counted, pred, aTv, cw_r, lane);
+    if (refine) refine_one<NPL>(lo, s, a.rl, a.R, counted, pred, aTv, cw_r, ctr_rp, lane);
 }
 
-template <int NPL>
+template <int NPL, int NR, bool INJECT>
 __global__ __launch_bounds__(256) void cache_step_kernel(Layout lo, StepArgs a) {
     const int lane = threadIdx.x & 63;
     const int s = blockIdx.x * kStreamsPerBlock + (threadIdx.x >> 6);
@@ -427,7 +452,7 @@ __global__ __launch_bounds__(256) void cache_step_kernel(Layout lo, StepArgs a) 
         // has completed) and is filled by the next one
         for (int i = threadIdx.x; i < lo.N; i += blockDim.x) lo.bcount[(int64_t)(a.bbuf ^ 1) * lo.N + i] = 0;
     }
-    if (s < lo.S) stream_step<NPL>(lo, a, s, lane);  // wave-uniform branch
+    if (s < lo.S) stream_step<NPL, NR, INJECT>(lo, a, s, lane);  // wave-uniform branch
 }
 
 // ---------------------------------------------------------------- init
@@ -449,6 +474,7 @@ __global__ void init_kernel(Layout lo) {
     for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.n_slots; i += gs) lo.slot_exp[i] = -1;
     for (int64_t i = gid; i < (int64_t)lo.L * lo.S * 4; i += gs) lo.events[i] = 0;
     for (int64_t i = gid; i < (int64_t)2 * lo.N; i += gs) lo.bcount[i] = 0;
+    for (int64_t i = gid; i < lo.N; i += gs) lo.zero_row[i] = 0.0f;
 }
 
 }  // namespace
@@ -458,15 +484,25 @@ hipError_t launch_init(const Layout& lo, hipStream_t st) {
     return hipGetLastError();
 }
 
-hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st) {
+template <int NPL, int NR>
+hipError_t launch_step_nr(const Layout& lo, const StepArgs& a, hipStream_t st) {
     const dim3 grid((lo.S + kStreamsPerBlock - 1) / kStreamsPerBlock);
-    if (lo.N <= 64)
-        hipLaunchKernelGGL(cache_step_kernel<1>, grid, dim3(256), 0, st, lo, a);
-    else if (lo.N <= 128)
-        hipLaunchKernelGGL(cache_step_kernel<2>, grid, dim3(256), 0, st, lo, a);
+    if (a.flags & kFlagInject)
+        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, true>), grid, dim3(256), 0, st, lo, a);
     else
-        hipLaunchKernelGGL(cache_step_kernel<4>, grid, dim3(256), 0, st, lo, a);
+        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, false>), grid, dim3(256), 0, st, lo, a);
     return hipGetLastError();
+}
+
+template <int NPL>
+hipError_t launch_step_npl(const Layout& lo, const StepArgs& a, hipStream_t st) {
+    return lo.n_r == 3 ? launch_step_nr<NPL, 3>(lo, a, st) : launch_step_nr<NPL, 2>(lo, a, st);
+}
+
+hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st) {
+    if (lo.N <= 64) return launch_step_npl<1>(lo, a, st);
+    if (lo.N <= 128) return launch_step_npl<2>(lo, a, st);
+    return launch_step_npl<4>(lo, a, st);
 }
 
 }  // namespace cmoe

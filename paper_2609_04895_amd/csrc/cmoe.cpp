@@ -81,7 +81,7 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
 // Offsets of every sub-buffer; used both for sizing and for carving.
 struct Plan {
     size_t cache, aT, pS, ctr, phys, active_sum, slot_of, slot_exp, state_total;
-    size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, ws_total;
+    size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, zero_row, ws_total;
     size_t arena;
 };
 
@@ -104,7 +104,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.slot_exp = take(2 * L * (size_t)dv.n_slots * 4);
     p.state_total = o;
     o = 0;
-    p.zpart = take(S * dv.n_r * N * (size_t)dv.nsplit * 8);
+    p.zpart = take(S * dv.n_r * N * (size_t)cmoe::kMaxSplit * 8);
     p.logits = take(L * S * dv.n_r * N * 4);
     p.sel = take(L * S * K * 4);
     p.gates = take(L * S * K * 4);
@@ -114,6 +114,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.pairs = take(2 * N * S * 4);
     p.act = take(S * K * (size_t)c->F * dv.esz);
     p.yp = take(S * K * (size_t)c->d * 4);
+    p.zero_row = take(N * 4);
     p.ws_total = o;
     p.arena = L * (size_t)dv.n_slots * dv.expert_bytes;
     return p;
@@ -289,6 +290,25 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     for (const void* p : {buf->arena, buf->state, buf->workspace})
         if (reinterpret_cast<uintptr_t>(p) & 255) return fail(CMOE_ERR_INVALID_ARG, "buffers must be 256-byte aligned");
 
+    // The fill kernel reads the cold pool directly: resolve its device address
+    // (a pinned host pool must be hipHostMalloc memory) and refuse pointers the
+    // device cannot access rather than fault later.
+    const void* pool_dev = w->cold_pool;
+    if (cfg->pool_kind == CMOE_POOL_HOST_PINNED) {
+        void* dptr = nullptr;
+        if (hipHostGetDevicePointer(&dptr, const_cast<void*>(w->cold_pool), 0) != hipSuccess || !dptr) {
+            (void)hipGetLastError();
+            return fail(CMOE_ERR_INVALID_ARG, "cold_pool is not pinned, device-mapped host memory");
+        }
+        pool_dev = dptr;
+    } else {
+        hipPointerAttribute_t attr;
+        if (hipPointerGetAttributes(&attr, w->cold_pool) != hipSuccess || attr.type != hipMemoryTypeDevice) {
+            (void)hipGetLastError();
+            return fail(CMOE_ERR_INVALID_ARG, "cold_pool is not device memory (use CMOE_POOL_HOST_PINNED for host)");
+        }
+    }
+
     cmoe_handle* hd = new cmoe_handle();
     hd->cfg = *cfg;
     hd->dv = dv;
@@ -305,7 +325,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.mode = cfg->mode; lo.dtype = cfg->dtype; lo.NW = dv.NW; lo.n_slots = dv.n_slots; lo.n_r = dv.n_r;
     lo.nsplit = dv.nsplit; lo.rdk = dv.rdk; lo.warmup = cfg->warmup_tokens;
     lo.expert_elems = (int64_t)3 * cfg->d * cfg->F;
-    lo.wR = w->w_router; lo.wT = w->w_temporal; lo.wS = w->w_spatio; lo.bias = w->logit_bias; lo.pool = w->cold_pool;
+    lo.wR = w->w_router; lo.wT = w->w_temporal; lo.wS = w->w_spatio; lo.bias = w->logit_bias; lo.pool = pool_dev;
     lo.arena = buf->arena;
     char* sb = static_cast<char*>(buf->state);
     char* wb = static_cast<char*>(buf->workspace);
@@ -327,6 +347,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.pairs = reinterpret_cast<int32_t*>(wb + p.pairs);
     lo.act = wb + p.act;
     lo.yp = reinterpret_cast<float*>(wb + p.yp);
+    lo.zero_row = reinterpret_cast<float*>(wb + p.zero_row);
 
     auto mk = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
     hd->ev_access.resize(cfg->L);

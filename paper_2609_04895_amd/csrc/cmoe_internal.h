@@ -37,7 +37,7 @@ struct Layout {
     int32_t* slot_of;           // [2][L][N]   slot of each expert, -1 absent (two versions)
     int32_t* slot_exp;          // [2][L][n_slots] expert in each slot, -1 free
     // workspace
-    double* zpart;              // [S][n_r][N][nsplit] router partial sums
+    double* zpart;              // [S][n_r][N][kMaxSplit] router partial sums
     float* logits;              // [L][S][n_r][N]
     int32_t* sel;               // [L][S][K]
     float* gates;               // [L][S][K]
@@ -47,6 +47,7 @@ struct Layout {
     int32_t* pairs;             // [2][N][S]   (stream << 8) | k of each token of an expert
     void* act;                  // [S][K][F]   SwiGLU intermediate (dtype)
     float* yp;                  // [S][K][d]   gated expert outputs
+    float* zero_row;            // [N]         zeros (native bias when there is none)
 };
 
 // cache-step kernel flags

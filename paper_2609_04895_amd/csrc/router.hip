@@ -83,15 +83,16 @@ __global__ __launch_bounds__(64) void router_kernel(Layout lo, int l, const void
     }
     // Output of the fp64 16x16x4 MFMA: lane (r16, g) holds D[g + 4 q][r16] in
     // acc[q], i.e. expert row g + 4 q of the tile, stream column r16.  The
-    // partial of split p goes to zpart[s][r][e][p]: the splits of one logit
-    // are contiguous for the cache-step kernel, which adds them in order.
+    // partial of split p goes to zpart[s][r][e][p] (p padded to kMaxSplit):
+    // the splits of one logit are contiguous for the cache-step kernel, which
+    // adds them in order.
     const int s = st * 16 + r16;
     if (s < lo.S) {
-        double* out = lo.zpart + ((int64_t)s * lo.n_r + r) * lo.N * lo.nsplit + p;
+        double* out = lo.zpart + ((int64_t)s * lo.n_r + r) * lo.N * kMaxSplit + p;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = et * 16 + g + 4 * q;
-            if (e < lo.N) out[(int64_t)e * lo.nsplit] = acc[q];
+            if (e < lo.N) out[(int64_t)e * kMaxSplit] = acc[q];
         }
     }
 }

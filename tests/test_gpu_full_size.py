@@ -1,0 +1,134 @@
+"""Parity at the workloads' full sizes, in the launch configuration bench.py
+times (side stream for proactive fills, all streams, all layers).
+
+The oracle replays the sampled streams {0, S-1} from the host twin's inputs
+(streams never interact in the logical cache path, so a stream replayed alone
+is exact): logits within one ulp, decisions, per-token events and the
+per-(stream, layer) counters bit for bit, and FFN outputs of sampled
+(stream, token, layer) triples within the bf16 tolerance.  For all streams the
+invariants that hold at any size are checked on every token: hits + demand
+misses = K, |C| <= capacity, proactive loads <= R (= 0 in update-only mode),
+traffic = (D + P) x expert bytes, physical fills <= D + P.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def run_full(w, T, ffn_samples=8, seed=0):
+    from paper_2609_04895_amd import cmoe as B
+    from paper_2609_04895_amd.workload import engine_for
+    say(f"full-size parity {w.name}: L={w.L} N={w.N} K={w.K} d={w.d} F={w.F} C={w.C} R={w.R} S={w.S}, {T} tokens")
+    inp = synth.device_inputs(w, T=T)
+    eng = engine_for(w, inp)
+    y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
+    full = w.mode == synth.MODE_SPATIO_TEMPORAL
+    n_r = 3 if full else 2
+    streams = [0, w.S - 1] if w.S > 1 else [0]
+    WR = [synth.router_host(w, synth.KIND_ROUTER_NATIVE, l) for l in range(w.L)]
+    WT = [synth.router_host(w, synth.KIND_ROUTER_TEMPORAL, l) for l in range(w.L)]
+    WS = [synth.router_host(w, synth.KIND_ROUTER_SPATIO, l) for l in range(w.L)] if full else None
+    bias = synth.zipf_bias(w)
+    H = {(s, l): synth.hidden_host(w, s, l, T=T) for s in streams for l in range(w.L)}
+    run = oracle.Run(w.L, w.N, w.K, w.C, w.R, len(streams), w.mode)
+    rng = np.random.default_rng(seed)
+    ffn_at = {(int(rng.integers(T)), int(rng.integers(len(streams))), int(rng.integers(w.L)))
+              for _ in range(ffn_samples)}
+    ulp_diffs = 0
+    worst = 0.0
+    experts = {}
+    for t in range(T):
+        eng.cmoe_step(inp["hidden"][t], y)
+        zg_all = eng.cmoe_read(B.CMOE_VIEW_LOGITS)               # [L][S][n_r][N]
+        zg = zg_all[:, streams].transpose(1, 0, 2, 3)            # [2][L][n_r][N]
+        for i, s in enumerate(streams):
+            for l in range(w.L):
+                h = H[(s, l)][t]
+                ref = [oracle.logits(WR[l], h, None if bias is None else bias[l]), oracle.logits(WT[l], h)]
+                if full:
+                    ref.append(oracle.logits(WS[l], h))
+                for r in range(n_r):
+                    d = zg[i, l, r] != ref[r]
+                    if d.any():
+                        gap = np.abs(zg[i, l, r].astype(np.float64) - ref[r])
+                        assert np.all(gap <= np.spacing(np.abs(ref[r]))), f"token {t} stream {s} layer {l}"
+                        ulp_diffs += int(d.sum())
+        out = run.step(zg[:, :, 0], zg[:, :, 1], zg[:, :, 2] if full else None, want="all")
+        sel = eng.cmoe_read(B.CMOE_VIEW_SELECTED)                 # [L][S][K]
+        assert np.array_equal(sel[:, streams].transpose(1, 0, 2), out["sel"]), f"token {t}: selections"
+        cache = eng.cache_sets()                                   # [S][L][N]
+        assert np.array_equal(cache[streams], run.cache.astype(bool)), f"token {t}: caches"
+        ev = eng.cmoe_read(B.CMOE_VIEW_EVENTS)                    # [L][S][4]
+        assert np.array_equal(ev[:, streams, 0].T, out["hits"])
+        assert np.array_equal(ev[:, streams, 1].T, out["nD"])
+        assert np.array_equal(ev[:, streams, 2].T, out["nP"])
+        # invariants over all streams
+        assert np.all(ev[:, :, 0] + ev[:, :, 1] == w.K), f"token {t}: hits + misses != K"
+        assert np.all(cache.sum(axis=-1) <= w.C), f"token {t}: cache over capacity"
+        assert np.all(ev[:, :, 2] <= (w.R if full else 0)), f"token {t}: too many proactive loads"
+        for (tt, i, l) in ffn_at:
+            if tt != t:
+                continue
+            s = streams[i]
+            yg = y[s, l].cpu().numpy()
+            ex = []
+            for e in out["sel"][i, l]:
+                key = (l, int(e))
+                if key not in experts:
+                    experts[key] = synth.expert_host(w, l, int(e))
+                ex.append(experts[key])
+            ref = oracle.moe_ffn(np.stack([a for a, _, _ in ex]), np.stack([b for _, b, _ in ex]),
+                                 np.stack([c for _, _, c in ex]), out["gate"][i, l], H[(s, l)][t])
+            err = rel_err(yg, ref)
+            worst = max(worst, err)
+            assert err <= 2e-2, f"token {t} stream {s} layer {l}: FFN relative error {err}"
+    tot, per, phys = eng.cmoe_stats()
+    assert np.array_equal(per[streams], run.ctr), "per-(stream, layer) counters"
+    assert tot["accesses"] == w.S * w.L * T * w.K
+    assert tot["hits"] + tot["demand_misses"] == tot["accesses"]
+    assert tot["tokens"] == w.S * T
+    assert tot["traffic_bytes"] == (tot["demand_misses"] + tot["proactive_loads"]) * w.expert_bytes
+    assert tot["phys_fills"] <= tot["demand_misses"] + tot["proactive_loads"]
+    if not full or w.R == 0:
+        assert tot["proactive_loads"] == 0
+    say(f"{w.name}: ok; one-ulp logit differences {ulp_diffs}; worst FFN error {worst:.3g}; "
+        f"hit {1 - tot['demand_misses'] / tot['accesses']:.4f}; proactive {tot['proactive_loads']}; "
+        f"physical fills {tot['phys_fills']}")
+    eng.cmoe_destroy()
+    del inp, eng
+    torch.cuda.empty_cache()
+
+
+def test_full_size_qwen3_30b_update_only():
+    run_full(synth.WORKLOADS["qwen3_30b"], T=24)
+
+
+def test_full_size_gptoss_20b_full_mode():
+    run_full(synth.WORKLOADS["gptoss_20b"], T=24)
+
+
+@pytest.mark.parametrize("C,R", [(16, 0), (32, 2), (64, 4)])
+def test_full_size_qwen3_30b_zipf_sweep_points(C, R):
+    run_full(synth.WORKLOADS["qwen3_30b_zipf"].replace(C=C, R=R), T=10, ffn_samples=4)
+
+
+PINNED_CAP_GB = 64 * 2 ** 30 / 1e9   # pinned host memory one process may hold on the GPU machine (measured)
+
+
+def test_full_size_qwen3_235b_slice_host_pool():
+    """Qwen3-235B-A22B-shaped slice with its cold pool in pinned host memory.
+
+    The full 16-layer pool is 77.3 GB; the GPU machine lets one process pin at most
+    64 GiB, so the test keeps as many layers as fit (12: 58.0 GB), every other
+    dimension at full size."""
+    w = synth.WORKLOADS["qwen3_235b_slice"]
+    per_layer = w.N * w.expert_bytes / 1e9
+    L = min(w.L, int(0.85 * PINNED_CAP_GB // per_layer))
+    run_full(w.replace(L=L), T=8, ffn_samples=4)
