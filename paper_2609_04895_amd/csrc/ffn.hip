@@ -28,14 +28,25 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kNG = 4;   // token groups (of 16) per pass over the weights
-constexpr int kUnroll = 4;
+constexpr int kNG = 4;          // token groups (of 16) per pass when a bucket holds more than 16
+constexpr int kUnroll = 4;      // k chunks per load block, one token group
+constexpr int kUnrollWide = 2;  // k chunks per load block, kNG token groups
 
 __device__ inline bf16x8 as_bf16x8(uint4 v) {
     bf16x8 r;
     __builtin_memcpy(&r, &v, 16);
     return r;
+}
+
+// Expert weights are read once per layer step and never again from cache:
+// stream them with nontemporal loads (measured on MI355X for this access
+// pattern, one contiguous block per wavefront: 7.0 TB/s against 6.1 TB/s
+// for ordinary loads).
+__device__ inline uint4 load_stream(const uint4* p) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return uint4{v.x, v.y, v.z, v.w};
 }
 
 __device__ inline f32x4 mfma_bf16(uint4 a, uint4 b, f32x4 c) {
@@ -52,111 +63,153 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
     return (a >> 16) | (b & 0xFFFF0000u);
 }
 
-// Weights of expert e of layer l in its HBM slot (slot map version sv), or
-// nullptr if it has none (cannot happen for a selected expert: the residency
-// step maps every member of any cache, and selected experts are members).
-__device__ inline const uint16_t* expert_base(const Layout& lo, int l, int sv, int e) {
+// Slot of expert e of layer l (slot map version sv), or -1 if it has none
+// (cannot happen for a selected expert: the residency step maps every member
+// of any cache, and selected experts are members).
+__device__ inline int expert_slot(const Layout& lo, int l, int sv, int e) {
     const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
-    if (slot < 0 || slot >= lo.n_slots) return nullptr;
+    return (slot < 0 || slot >= lo.n_slots) ? -1 : slot;
+}
+
+__device__ inline const uint16_t* slot_base(const Layout& lo, int l, int slot) {
     return reinterpret_cast<const uint16_t*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems;
 }
 
-// ---------------------------------------------------------------- bf16
-__global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, int bbuf, int sv, const uint16_t* __restrict__ h) {
-    const int ftn = lo.F / 16;
-    const int e = blockIdx.x / ftn, ft = blockIdx.x - e * ftn;
-    const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
-    if (m == 0) return;
-    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
-    const uint16_t* Wg = expert_base(lo, l, sv, e);
-    if (!Wg) return;
-    const int lane = threadIdx.x, r = lane & 15, g = lane >> 4;
-    // packed slot layout: chunk c of this row tile is 256 units of 16 bytes,
-    // gate half 0, gate half 1, up half 0, up half 1, each 64 units
-    const uint4* tileA = reinterpret_cast<const uint4*>(Wg) + (int64_t)ft * (lo.d / 64) * 256 + lane;
-    uint16_t* act = reinterpret_cast<uint16_t*>(lo.act);
-    const int d = lo.d;
-    const int nchunk = d / 64;
+// U consecutive 64-wide k chunks of one 16-row (gate/up) or 2 x 16-row (down)
+// weight tile against NG groups of 16 token columns.  All weight and
+// activation loads of the block are issued before the first matrix-core
+// instruction, so a wavefront waits once per block.  Token columns past the
+// bucket (also whole groups past it in the last pass) repeat the bucket's last
+// token and their output columns are discarded: column j of the product
+// depends on column j of B only.
+template <int NG, int U>
+__device__ inline void mfma_block(const uint4* __restrict__ tile, int c, const uint16_t* const* xb, f32x4* acc0,
+                                  f32x4* acc1) {
+    uint4 A[U][4], X[NG][U][2];
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+        const uint4* ch = tile + (int64_t)(c + i) * 256;
+        A[i][0] = load_stream(ch);
+        A[i][1] = load_stream(ch + 64);
+        A[i][2] = load_stream(ch + 128);
+        A[i][3] = load_stream(ch + 192);
+    }
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+#pragma unroll
+        for (int i = 0; i < U; ++i) {
+            const int kc = (c + i) * 64;
+            X[q][i][0] = *reinterpret_cast<const uint4*>(xb[q] + kc);
+            X[q][i][1] = *reinterpret_cast<const uint4*>(xb[q] + kc + 8);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep every load of the block ahead of the matrix-core work
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+#pragma unroll
+        for (int i = 0; i < U; ++i) {
+            acc0[q] = mfma_bf16(A[i][0], X[q][i][0], acc0[q]);
+            acc0[q] = mfma_bf16(A[i][1], X[q][i][1], acc0[q]);
+            acc1[q] = mfma_bf16(A[i][2], X[q][i][0], acc1[q]);
+            acc1[q] = mfma_bf16(A[i][3], X[q][i][1], acc1[q]);
+        }
+    }
+}
 
-    for (int t0 = 0; t0 < m; t0 += 16 * kNG) {
-        const int ng = min(kNG, (m - t0 + 15) / 16);
-        const uint16_t* xb[kNG];
-        bool xv[kNG];
+// The k loop of one pass: blocks of U chunks, then single chunks.
+template <int NG, int U>
+__device__ inline void mfma_pass(const uint4* __restrict__ tile, int nchunk, const uint16_t* const* xb, f32x4* acc0,
+                                 f32x4* acc1) {
 #pragma unroll
-        for (int q = 0; q < kNG; ++q) {
-            const int tok = t0 + 16 * q + r;
-            xv[q] = q < ng && tok < m;
-            const int s = xv[q] ? (bk[tok] >> 8) : 0;
-            xb[q] = h + ((int64_t)s * lo.L + l) * d + 16 * g;
-        }
-        f32x4 cg[kNG], cu[kNG];
+    for (int q = 0; q < NG; ++q) {
+        acc0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    int c = 0;
+    for (; c + U <= nchunk; c += U) mfma_block<NG, U>(tile, c, xb, acc0, acc1);
+    for (; c < nchunk; ++c) mfma_block<NG, 1>(tile, c, xb, acc0, acc1);
+}
+
+// ---------------------------------------------------------------- bf16
+// Token groups of one pass over the weights: one group (up to 16 tokens, the
+// common case) with a deep k block, or kNG groups with a shallower one.
+template <int NG, int U>
+__device__ inline void up_passes(const Layout& lo, int l, int ft, const int32_t* __restrict__ bk, int m,
+                                 const uint4* __restrict__ tileA, const uint16_t* __restrict__ h, int lane) {
+    const int r = lane & 15, g = lane >> 4;
+    const int d = lo.d;
+    uint16_t* act = reinterpret_cast<uint16_t*>(lo.act);
+    for (int t0 = 0; t0 < m; t0 += 16 * NG) {
+        const int ng = min(NG, (m - t0 + 15) / 16);
+        int pr[NG];
+        const uint16_t* xb[NG];
 #pragma unroll
-        for (int q = 0; q < kNG; ++q) {
-            cg[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-            cu[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-        int c = 0;
-        for (; c + kUnroll <= nchunk; c += kUnroll) {
-            uint4 G[kUnroll][2], U[kUnroll][2];
+        for (int q = 0; q < NG; ++q) pr[q] = bk[min(t0 + 16 * q + r, m - 1)];
 #pragma unroll
-            for (int i = 0; i < kUnroll; ++i) {
-                const uint4* ch = tileA + (int64_t)(c + i) * 256;
-                G[i][0] = ch[0];
-                G[i][1] = ch[64];
-                U[i][0] = ch[128];
-                U[i][1] = ch[192];
-            }
-#pragma unroll
-            for (int q = 0; q < kNG; ++q) {
-                if (q >= ng) break;
-#pragma unroll
-                for (int i = 0; i < kUnroll; ++i) {
-                    const int kc = (c + i) * 64;
-                    uint4 x0 = {0, 0, 0, 0}, x1 = {0, 0, 0, 0};
-                    if (xv[q]) {
-                        x0 = *reinterpret_cast<const uint4*>(xb[q] + kc);
-                        x1 = *reinterpret_cast<const uint4*>(xb[q] + kc + 8);
-                    }
-                    cg[q] = mfma_bf16(G[i][0], x0, cg[q]);
-                    cg[q] = mfma_bf16(G[i][1], x1, cg[q]);
-                    cu[q] = mfma_bf16(U[i][0], x0, cu[q]);
-                    cu[q] = mfma_bf16(U[i][1], x1, cu[q]);
-                }
-            }
-        }
-        for (; c < nchunk; ++c) {
-            const int kc = c * 64;
-            const uint4* ch = tileA + (int64_t)c * 256;
-            const uint4 g0 = ch[0];
-            const uint4 g1 = ch[64];
-            const uint4 u0 = ch[128];
-            const uint4 u1 = ch[192];
-#pragma unroll
-            for (int q = 0; q < kNG; ++q) {
-                if (q >= ng) break;
-                uint4 x0 = {0, 0, 0, 0}, x1 = {0, 0, 0, 0};
-                if (xv[q]) {
-                    x0 = *reinterpret_cast<const uint4*>(xb[q] + kc);
-                    x1 = *reinterpret_cast<const uint4*>(xb[q] + kc + 8);
-                }
-                cg[q] = mfma_bf16(g0, x0, cg[q]);
-                cg[q] = mfma_bf16(g1, x1, cg[q]);
-                cu[q] = mfma_bf16(u0, x0, cu[q]);
-                cu[q] = mfma_bf16(u1, x1, cu[q]);
-            }
-        }
+        for (int q = 0; q < NG; ++q) xb[q] = h + ((int64_t)(pr[q] >> 8) * lo.L + l) * d + 16 * g;
+        f32x4 cg[NG], cu[NG];
+        mfma_pass<NG, U>(tileA, d / 64, xb, cg, cu);
         // D[i][j]: row i = 4 g + rr of this 16-row tile, token column j = r
 #pragma unroll
-        for (int q = 0; q < kNG; ++q) {
+        for (int q = 0; q < NG; ++q) {
             if (q >= ng) break;
             const int tok = t0 + 16 * q + r;
             if (tok < m) {
                 uint2 o;
                 o.x = pack_bf16x2(silu_mul(cg[q][0], cu[q][0]), silu_mul(cg[q][1], cu[q][1]));
                 o.y = pack_bf16x2(silu_mul(cg[q][2], cu[q][2]), silu_mul(cg[q][3], cu[q][3]));
-                const int pair = bk[tok];
+                const int pair = pr[q];
                 const int64_t row = (int64_t)(pair >> 8) * lo.K + (pair & 255);  // token (s, k)
                 *reinterpret_cast<uint2*>(act + row * lo.F + ft * 16 + 4 * g) = o;
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, int bbuf, int sv, const uint16_t* __restrict__ h) {
+    const int ftn = lo.F / 16;
+    const int e = blockIdx.x / ftn, ft = blockIdx.x - e * ftn;
+    const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
+    const int slot = expert_slot(lo, l, sv, e);
+    if (m == 0 || slot < 0) return;
+    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
+    // packed slot layout: chunk c of this row tile is 256 units of 16 bytes,
+    // gate half 0, gate half 1, up half 0, up half 1, each 64 units
+    const uint4* tileA =
+        reinterpret_cast<const uint4*>(slot_base(lo, l, slot)) + (int64_t)ft * (lo.d / 64) * 256 + threadIdx.x;
+    if (m <= 16)
+        up_passes<1, kUnroll>(lo, l, ft, bk, m, tileA, h, threadIdx.x);
+    else
+        up_passes<kNG, kUnrollWide>(lo, l, ft, bk, m, tileA, h, threadIdx.x);
+}
+
+template <int NG, int U>
+__device__ inline void down_passes(const Layout& lo, int l, int dt, const int32_t* __restrict__ bk, int m,
+                                   const uint4* __restrict__ tileB, int lane) {
+    const int r = lane & 15, g = lane >> 4;
+    const int F = lo.F;
+    const uint16_t* act = reinterpret_cast<const uint16_t*>(lo.act);
+    for (int t0 = 0; t0 < m; t0 += 16 * NG) {
+        const int ng = min(NG, (m - t0 + 15) / 16);
+        int pr[NG];
+        const uint16_t* xb[NG];
+#pragma unroll
+        for (int q = 0; q < NG; ++q) pr[q] = bk[min(t0 + 16 * q + r, m - 1)];
+#pragma unroll
+        for (int q = 0; q < NG; ++q) xb[q] = act + ((int64_t)(pr[q] >> 8) * lo.K + (pr[q] & 255)) * F + 16 * g;
+        f32x4 c0[NG], c1[NG];
+        mfma_pass<NG, U>(tileB, F / 64, xb, c0, c1);
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            if (q >= ng) break;
+            const int tok = t0 + 16 * q + r;
+            if (tok < m) {
+                const int s = pr[q] >> 8, k = pr[q] & 255;
+                const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
+                float* dst = lo.yp + ((int64_t)s * lo.K + k) * lo.d + dt * 32 + 4 * g;
+                *reinterpret_cast<float4*>(dst) = make_float4(gk * c0[q][0], gk * c0[q][1], gk * c0[q][2], gk * c0[q][3]);
+                *reinterpret_cast<float4*>(dst + 16) =
+                    make_float4(gk * c1[q][0], gk * c1[q][1], gk * c1[q][2], gk * c1[q][3]);
             }
         }
     }
@@ -166,102 +219,18 @@ __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l, int bbuf, 
     const int dtn = lo.d / 32;
     const int e = blockIdx.x / dtn, dt = blockIdx.x - e * dtn;
     const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
-    if (m == 0) return;
+    const int slot = expert_slot(lo, l, sv, e);
+    if (m == 0 || slot < 0) return;
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
-    const int F = lo.F;
-    const uint16_t* Wbase = expert_base(lo, l, sv, e);
-    if (!Wbase) return;
-    const int lane = threadIdx.x, r = lane & 15, g = lane >> 4;
     // packed slot layout: after the gate/up part (F d / 4 units), chunk c of
     // this 32-row tile is 256 units: rows 0-15 half 0, half 1, rows 16-31
     // half 0, half 1, each 64 units
-    const uint4* tileB =
-        reinterpret_cast<const uint4*>(Wbase) + (int64_t)F * lo.d / 4 + (int64_t)dt * (F / 64) * 256 + lane;
-    const uint16_t* act = reinterpret_cast<const uint16_t*>(lo.act);
-    const int nchunk = F / 64;
-
-    for (int t0 = 0; t0 < m; t0 += 16 * kNG) {
-        const int ng = min(kNG, (m - t0 + 15) / 16);
-        const uint16_t* xb[kNG];
-        bool xv[kNG];
-#pragma unroll
-        for (int q = 0; q < kNG; ++q) {
-            const int tok = t0 + 16 * q + r;
-            xv[q] = q < ng && tok < m;
-            const int pair = xv[q] ? bk[tok] : 0;
-            xb[q] = act + ((int64_t)(pair >> 8) * lo.K + (pair & 255)) * F + 16 * g;
-        }
-        f32x4 c0[kNG], c1[kNG];
-#pragma unroll
-        for (int q = 0; q < kNG; ++q) {
-            c0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-            c1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-        int c = 0;
-        for (; c + kUnroll <= nchunk; c += kUnroll) {
-            uint4 A0[kUnroll][2], A1[kUnroll][2];
-#pragma unroll
-            for (int i = 0; i < kUnroll; ++i) {
-                const uint4* ch = tileB + (int64_t)(c + i) * 256;
-                A0[i][0] = ch[0];
-                A0[i][1] = ch[64];
-                A1[i][0] = ch[128];
-                A1[i][1] = ch[192];
-            }
-#pragma unroll
-            for (int q = 0; q < kNG; ++q) {
-                if (q >= ng) break;
-#pragma unroll
-                for (int i = 0; i < kUnroll; ++i) {
-                    const int kc = (c + i) * 64;
-                    uint4 x0 = {0, 0, 0, 0}, x1 = {0, 0, 0, 0};
-                    if (xv[q]) {
-                        x0 = *reinterpret_cast<const uint4*>(xb[q] + kc);
-                        x1 = *reinterpret_cast<const uint4*>(xb[q] + kc + 8);
-                    }
-                    c0[q] = mfma_bf16(A0[i][0], x0, c0[q]);
-                    c0[q] = mfma_bf16(A0[i][1], x1, c0[q]);
-                    c1[q] = mfma_bf16(A1[i][0], x0, c1[q]);
-                    c1[q] = mfma_bf16(A1[i][1], x1, c1[q]);
-                }
-            }
-        }
-        for (; c < nchunk; ++c) {
-            const int kc = c * 64;
-            const uint4* ch = tileB + (int64_t)c * 256;
-            const uint4 p0 = ch[0];
-            const uint4 p1 = ch[64];
-            const uint4 q0 = ch[128];
-            const uint4 q1 = ch[192];
-#pragma unroll
-            for (int q = 0; q < kNG; ++q) {
-                if (q >= ng) break;
-                uint4 x0 = {0, 0, 0, 0}, x1 = {0, 0, 0, 0};
-                if (xv[q]) {
-                    x0 = *reinterpret_cast<const uint4*>(xb[q] + kc);
-                    x1 = *reinterpret_cast<const uint4*>(xb[q] + kc + 8);
-                }
-                c0[q] = mfma_bf16(p0, x0, c0[q]);
-                c0[q] = mfma_bf16(p1, x1, c0[q]);
-                c1[q] = mfma_bf16(q0, x0, c1[q]);
-                c1[q] = mfma_bf16(q1, x1, c1[q]);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < kNG; ++q) {
-            if (q >= ng) break;
-            const int tok = t0 + 16 * q + r;
-            if (tok < m) {
-                const int pair = bk[tok];
-                const int s = pair >> 8, k = pair & 255;
-                const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
-                float* dst = lo.yp + ((int64_t)s * lo.K + k) * lo.d + dt * 32 + 4 * g;
-                *reinterpret_cast<float4*>(dst) = make_float4(gk * c0[q][0], gk * c0[q][1], gk * c0[q][2], gk * c0[q][3]);
-                *reinterpret_cast<float4*>(dst + 16) =
-                    make_float4(gk * c1[q][0], gk * c1[q][1], gk * c1[q][2], gk * c1[q][3]);
-            }
-        }
-    }
+    const uint4* tileB = reinterpret_cast<const uint4*>(slot_base(lo, l, slot)) + (int64_t)lo.F * lo.d / 4 +
+                         (int64_t)dt * (lo.F / 64) * 256 + threadIdx.x;
+    if (m <= 16)
+        down_passes<1, kUnroll>(lo, l, dt, bk, m, tileB, threadIdx.x);
+    else
+        down_passes<kNG, kUnrollWide>(lo, l, dt, bk, m, tileB, threadIdx.x);
 }
 
 // ---------------------------------------------------------------- fp32
