@@ -79,28 +79,109 @@ __device__ inline uint32_t ord32(float x) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Cross-lane steps without the LDS crossbar (all 64 lanes active):
+// DPP quad permutations and mirrors inside 16-lane rows, and the gfx950
+// permlane swaps across rows.  permlane16_swap(x, x) returns, in every lane,
+// the pair {own value, value of lane ^ 16} in some order (permlane32_swap:
+// lane ^ 32), so an order-free combine of the pair is the combine with that
+// partner.
+template <int CTRL>
+__device__ inline unsigned dpp(unsigned v) {
+    return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xF, 0xF, false);
+}
+constexpr int kQuadXor1 = 0xB1;     // quad_perm 1,0,3,2
+constexpr int kQuadXor2 = 0x4E;     // quad_perm 2,3,0,1
+constexpr int kRowHalfMirror = 0x141;
+constexpr int kRowMirror = 0x140;
+constexpr int kRowShl1 = 0x101;     // lane i reads lane i + n of its row
+
+__device__ inline unsigned long long pack64(unsigned hi, unsigned lo) {
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+template <int CTRL>
+__device__ inline unsigned long long dpp64(unsigned long long v) {
+    return pack64(dpp<CTRL>((unsigned)(v >> 32)), dpp<CTRL>((unsigned)v));
+}
+
+// {v of this lane, v of lane ^ 16} and {v of this lane, v of lane ^ 32}
+__device__ inline void swap16_64(unsigned long long v, unsigned long long& a, unsigned long long& b) {
+    const auto h = __builtin_amdgcn_permlane16_swap((unsigned)(v >> 32), (unsigned)(v >> 32), false, false);
+    const auto l = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+    a = pack64(h[0], l[0]);
+    b = pack64(h[1], l[1]);
+}
+__device__ inline void swap32_64(unsigned long long v, unsigned long long& a, unsigned long long& b) {
+    const auto h = __builtin_amdgcn_permlane32_swap((unsigned)(v >> 32), (unsigned)(v >> 32), false, false);
+    const auto l = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+    a = pack64(h[0], l[0]);
+    b = pack64(h[1], l[1]);
+}
+
+__device__ inline unsigned long long max64(unsigned long long a, unsigned long long b) { return a > b ? a : b; }
+__device__ inline unsigned long long min64(unsigned long long a, unsigned long long b) { return a < b ? a : b; }
+
+__device__ inline unsigned long long uniform64(unsigned long long v) {
+    return pack64(__builtin_amdgcn_readfirstlane((unsigned)(v >> 32)), __builtin_amdgcn_readfirstlane((unsigned)v));
+}
+
+// maximum over the wavefront, returned as a wave-uniform value
 __device__ inline unsigned long long wave_max_u64(unsigned long long v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const unsigned long long w = __shfl_xor(v, o);
-        v = w > v ? w : v;
-    }
-    return v;
+    v = max64(v, dpp64<kQuadXor1>(v));
+    v = max64(v, dpp64<kQuadXor2>(v));
+    v = max64(v, dpp64<kRowHalfMirror>(v));
+    v = max64(v, dpp64<kRowMirror>(v));
+    unsigned long long a, b;
+    swap16_64(v, a, b);
+    v = max64(a, b);
+    swap32_64(v, a, b);
+    return uniform64(max64(a, b));
 }
 
 __device__ inline unsigned long long wave_min_u64(unsigned long long v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const unsigned long long w = __shfl_xor(v, o);
-        v = w < v ? w : v;
-    }
-    return v;
+    v = min64(v, dpp64<kQuadXor1>(v));
+    v = min64(v, dpp64<kQuadXor2>(v));
+    v = min64(v, dpp64<kRowHalfMirror>(v));
+    v = min64(v, dpp64<kRowMirror>(v));
+    unsigned long long a, b;
+    swap16_64(v, a, b);
+    v = min64(a, b);
+    swap32_64(v, a, b);
+    return uniform64(min64(a, b));
 }
 
 __device__ inline float wave_max_f32(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-    return v;
+    unsigned u = __float_as_uint(v);
+    u = __float_as_uint(fmaxf(__uint_as_float(u), __uint_as_float(dpp<kQuadXor1>(u))));
+    u = __float_as_uint(fmaxf(__uint_as_float(u), __uint_as_float(dpp<kQuadXor2>(u))));
+    u = __float_as_uint(fmaxf(__uint_as_float(u), __uint_as_float(dpp<kRowHalfMirror>(u))));
+    u = __float_as_uint(fmaxf(__uint_as_float(u), __uint_as_float(dpp<kRowMirror>(u))));
+    const auto p = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    u = __float_as_uint(fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1])));
+    const auto q = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    u = __float_as_uint(fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1])));
+    return __uint_as_float(__builtin_amdgcn_readfirstlane(u));
+}
+
+// Strided-halving sum of lanes [0, P) for a power of two P <= 64: at
+// w = P/2 .. 1, lane i < w adds lane i + w (the tree of lane 0 is exactly
+// that order); returns lane 0's total to every lane.
+__device__ inline float wave_sum_halving(float x, int P) {
+    if (P >= 64) {
+        const unsigned u = __float_as_uint(x);
+        const auto q = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+        x = x + __uint_as_float(q[1]);  // lanes < 32: lane + 32
+    }
+    if (P >= 32) {
+        const unsigned u = __float_as_uint(x);
+        const auto q = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        x = x + __uint_as_float(q[1]);  // lanes of even rows: lane + 16
+    }
+    if (P >= 16) x = x + __uint_as_float(dpp<kRowShl1 + 7>(__float_as_uint(x)));
+    if (P >= 8) x = x + __uint_as_float(dpp<kRowShl1 + 3>(__float_as_uint(x)));
+    if (P >= 4) x = x + __uint_as_float(dpp<kRowShl1 + 1>(__float_as_uint(x)));
+    if (P >= 2) x = x + __uint_as_float(dpp<kRowShl1>(__float_as_uint(x)));
+    return __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 0));
 }
 
 template <int NPL>
@@ -128,12 +209,7 @@ __device__ inline void softmax_fixed(const float (&z)[NPL], int N, int lane, flo
         }
     }
     // cross-lane halving steps (w < 64)
-    float x = v[0];
-    for (int w = (P / 2 < 32 ? P / 2 : 32); w >= 1; w >>= 1) {
-        const float o = __shfl_down(x, w);
-        x = x + o;
-    }
-    const float sum = __shfl(x, 0);
+    const float sum = wave_sum_halving(v[0], P < 64 ? P : 64);
 #pragma unroll
     for (int j = 0; j < NPL; ++j) p[j] = p[j] / sum;
 }
@@ -351,7 +427,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
                     pv = pR[j];
                 }
             }
-            pv = __shfl(pv, e & 63);
+            pv = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(pv), e & 63));
             gsum = gsum + pv;
             set_bit(sw, e);
             if (lane == k) {
@@ -444,7 +520,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
 }
 
 template <int NPL, int NR, bool INJECT>
-__global__ __launch_bounds__(256) void cache_step_kernel(Layout lo, StepArgs a) {
+__global__ __launch_bounds__(64 * kStreamsPerBlock) void cache_step_kernel(Layout lo, StepArgs a) {
     const int lane = threadIdx.x & 63;
     const int s = blockIdx.x * kStreamsPerBlock + (threadIdx.x >> 6);
     if ((a.flags & kFlagAccess) && blockIdx.x == 0) {
@@ -488,9 +564,9 @@ template <int NPL, int NR>
 hipError_t launch_step_nr(const Layout& lo, const StepArgs& a, hipStream_t st) {
     const dim3 grid((lo.S + kStreamsPerBlock - 1) / kStreamsPerBlock);
     if (a.flags & kFlagInject)
-        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, true>), grid, dim3(256), 0, st, lo, a);
+        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, true>), grid, dim3(64 * kStreamsPerBlock), 0, st, lo, a);
     else
-        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, false>), grid, dim3(256), 0, st, lo, a);
+        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, false>), grid, dim3(64 * kStreamsPerBlock), 0, st, lo, a);
     return hipGetLastError();
 }
 

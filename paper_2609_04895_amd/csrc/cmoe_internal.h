@@ -12,7 +12,7 @@ constexpr int kCtrA = 0, kCtrHits = 1, kCtrD = 2, kCtrP = 3, kCtrT = 4;
 constexpr int kMaxN = 256;        // experts per layer handled by the kernels
 constexpr int kMaxK = 64;         // Top-K handled by the kernels (one lane per selected expert)
 constexpr int kMaxSplit = 16;     // router split-K parts
-constexpr int kStreamsPerBlock = 4;   // cache-step kernel: one wavefront per stream
+constexpr int kStreamsPerBlock = 1;   // cache-step kernel: one wavefront per stream
 constexpr int kFillBlocks = 128;  // fill kernel workgroups
 
 // Every pointer the kernels use, carved out of the caller's buffers.
