@@ -315,7 +315,7 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, bool counted,
     }
 }
 
-template <int NPL, int NR, bool INJECT>
+template <int NPL, int NR, bool INJECT, int ZS>
 __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane) {
     const int N = lo.N, L = lo.L, K = lo.K;
     const bool full = lo.mode == 1;
@@ -348,12 +348,12 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
     if (a.flags & kFlagAccess) {
         const int l = a.l;
         const int64_t sl = (int64_t)s * L + l;
-        // logits: every load is issued first (router split partials, padded to
-        // kMaxSplit per logit, or the injected logits; the native bias, a zero
-        // row when there is none), then the splits are added in ascending
-        // order and rounded once
+        // logits: every load is issued first (router split partials, ZS slots
+        // per logit, or the injected logits; the native bias, a zero row when
+        // there is none), then the splits are added in ascending order and
+        // rounded once
         const float* brow = lo.bias ? lo.bias + (int64_t)l * N : lo.zero_row;
-        double2 pv[NR][NPL][kMaxSplit / 2];
+        double2 pv[NR][NPL][ZS / 2];
         float zin[NR][NPL], bz[NPL];
 #pragma unroll
         for (int j = 0; j < NPL; ++j) {
@@ -367,9 +367,9 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
                     zin[r][j] = src[sl * N + ec];
                 } else {
                     const double2* zp =
-                        reinterpret_cast<const double2*>(lo.zpart + (((int64_t)s * NR + r) * N + ec) * kMaxSplit);
+                        reinterpret_cast<const double2*>(lo.zpart + (((int64_t)s * NR + r) * N + ec) * ZS);
 #pragma unroll
-                    for (int u = 0; u < kMaxSplit / 2; ++u) pv[r][j][u] = zp[u];
+                    for (int u = 0; u < ZS / 2; ++u) pv[r][j][u] = zp[u];
                 }
             }
         }
@@ -386,7 +386,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
                 } else {
                     double acc = 0.0;
 #pragma unroll
-                    for (int p = 0; p < kMaxSplit; ++p)
+                    for (int p = 0; p < ZS; ++p)
                         if (p < lo.nsplit) acc += (p & 1) ? pv[r][j][p >> 1].y : pv[r][j][p >> 1].x;
                     if (r == 0) acc += (double)bz[j];
                     v = (float)acc;
@@ -519,7 +519,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
     if (refine) refine_one<NPL>(lo, s, a.rl, a.R, counted, pred, aTv, cw_r, ctr_rp, lane);
 }
 
-template <int NPL, int NR, bool INJECT>
+template <int NPL, int NR, bool INJECT, int ZS>
 __global__ __launch_bounds__(64 * kStreamsPerBlock) void cache_step_kernel(Layout lo, StepArgs a) {
     const int lane = threadIdx.x & 63;
     const int s = blockIdx.x * kStreamsPerBlock + (threadIdx.x >> 6);
@@ -528,7 +528,7 @@ __global__ __launch_bounds__(64 * kStreamsPerBlock) void cache_step_kernel(Layou
         // has completed) and is filled by the next one
         for (int i = threadIdx.x; i < lo.N; i += blockDim.x) lo.bcount[(int64_t)(a.bbuf ^ 1) * lo.N + i] = 0;
     }
-    if (s < lo.S) stream_step<NPL, NR, INJECT>(lo, a, s, lane);  // wave-uniform branch
+    if (s < lo.S) stream_step<NPL, NR, INJECT, ZS>(lo, a, s, lane);  // wave-uniform branch
 }
 
 // ---------------------------------------------------------------- init
@@ -563,10 +563,13 @@ hipError_t launch_init(const Layout& lo, hipStream_t st) {
 template <int NPL, int NR>
 hipError_t launch_step_nr(const Layout& lo, const StepArgs& a, hipStream_t st) {
     const dim3 grid((lo.S + kStreamsPerBlock - 1) / kStreamsPerBlock);
+    const dim3 block(64 * kStreamsPerBlock);
     if (a.flags & kFlagInject)
-        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, true>), grid, dim3(64 * kStreamsPerBlock), 0, st, lo, a);
+        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, true, 2>), grid, block, 0, st, lo, a);
+    else if (lo.zstride == 4)
+        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, false, 4>), grid, block, 0, st, lo, a);
     else
-        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, false>), grid, dim3(64 * kStreamsPerBlock), 0, st, lo, a);
+        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, false, kMaxSplit>), grid, block, 0, st, lo, a);
     return hipGetLastError();
 }
 

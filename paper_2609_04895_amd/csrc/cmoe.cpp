@@ -41,7 +41,7 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 enum KernelId { KID_ROUTER = 0, KID_CACHE = 1, KID_FILL = 2, KID_UP = 3, KID_DOWN = 4, KID_COMBINE = 5 };
 
 struct Derived {
-    int NW, n_r, n_slots, nsplit, rdk;
+    int NW, n_r, n_slots, nsplit, rdk, zstride;
     size_t esz, expert_bytes;
 };
 
@@ -67,14 +67,19 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     dv->n_slots = (int)std::min<int64_t>(c->N, (int64_t)c->S * c->C);
     dv->esz = c->dtype == CMOE_BF16 ? 2 : 4;
     dv->expert_bytes = (size_t)3 * c->d * c->F * dv->esz;
-    // router split-K: 32-aligned chunks, at most kMaxSplit splits, as few as
+    // router split-K: each wavefront of a router workgroup sums a 32-aligned
+    // k range of rdk; a workgroup covers kRouterWaves ranges and writes one
+    // partial; at most kMaxSplit partials per logit, and ranges as long as
     // still give about a thousand wavefronts
     const int64_t tiles = (int64_t)dv->n_r * ((c->N + 15) / 16) * ((c->S + 15) / 16);
+    const int W = cmoe::kRouterWaves;
+    auto splits = [&](int64_t k) { return (c->d + W * k - 1) / (W * k); };
     int rdk = 32;
-    while (rdk < c->d && (c->d + rdk - 1) / rdk > cmoe::kMaxSplit) rdk *= 2;
-    while (rdk * 2 <= c->d && tiles * ((c->d + 2 * rdk - 1) / (2 * rdk)) >= 1024) rdk *= 2;
+    while (splits(rdk) > cmoe::kMaxSplit) rdk *= 2;
+    while (W * 2 * rdk <= c->d && tiles * W * splits(2 * rdk) >= 1024) rdk *= 2;
     dv->rdk = rdk;
-    dv->nsplit = (c->d + rdk - 1) / rdk;
+    dv->nsplit = (int)splits(rdk);
+    dv->zstride = dv->nsplit <= 4 ? 4 : cmoe::kMaxSplit;  // partial slots per logit
     return CMOE_OK;
 }
 
@@ -104,7 +109,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.slot_exp = take(2 * L * (size_t)dv.n_slots * 4);
     p.state_total = o;
     o = 0;
-    p.zpart = take(S * dv.n_r * N * (size_t)cmoe::kMaxSplit * 8);
+    p.zpart = take(S * dv.n_r * N * (size_t)dv.zstride * 8);
     p.logits = take(L * S * dv.n_r * N * 4);
     p.sel = take(L * S * K * 4);
     p.gates = take(L * S * K * 4);
@@ -323,7 +328,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     const Plan& p = hd->plan;
     lo.L = cfg->L; lo.N = cfg->N; lo.K = cfg->K; lo.d = cfg->d; lo.F = cfg->F; lo.C = cfg->C; lo.S = cfg->S;
     lo.mode = cfg->mode; lo.dtype = cfg->dtype; lo.NW = dv.NW; lo.n_slots = dv.n_slots; lo.n_r = dv.n_r;
-    lo.nsplit = dv.nsplit; lo.rdk = dv.rdk; lo.warmup = cfg->warmup_tokens;
+    lo.nsplit = dv.nsplit; lo.rdk = dv.rdk; lo.zstride = dv.zstride; lo.warmup = cfg->warmup_tokens;
     lo.expert_elems = (int64_t)3 * cfg->d * cfg->F;
     lo.wR = w->w_router; lo.wT = w->w_temporal; lo.wS = w->w_spatio; lo.bias = w->logit_bias; lo.pool = pool_dev;
     lo.arena = buf->arena;

@@ -11,13 +11,14 @@ constexpr int kNctr = 5;          // per (stream, layer) counters: A, hits, D, P
 constexpr int kCtrA = 0, kCtrHits = 1, kCtrD = 2, kCtrP = 3, kCtrT = 4;
 constexpr int kMaxN = 256;        // experts per layer handled by the kernels
 constexpr int kMaxK = 64;         // Top-K handled by the kernels (one lane per selected expert)
-constexpr int kMaxSplit = 16;     // router split-K parts
+constexpr int kMaxSplit = 16;        // router split-K partials per logit, at most
+constexpr int kRouterWaves = 4;      // router: wavefronts per workgroup, one k sub-range each
 constexpr int kStreamsPerBlock = 1;   // cache-step kernel: one wavefront per stream
 constexpr int kFillBlocks = 128;  // fill kernel workgroups
 
 // Every pointer the kernels use, carved out of the caller's buffers.
 struct Layout {
-    int32_t L, N, K, d, F, C, S, mode, dtype, NW, n_slots, n_r, nsplit, rdk, warmup;
+    int32_t L, N, K, d, F, C, S, mode, dtype, NW, n_slots, n_r, nsplit, rdk, zstride, warmup;
     int64_t expert_elems;  // 3 d F
     // weights
     const void* wR;
