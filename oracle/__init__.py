@@ -19,6 +19,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
 NCTR = 5  # A, hits, D, P, T
+MODE_TEMPORAL, MODE_SPATIO_TEMPORAL, MODE_SPATIO_ONLY = 0, 1, 2
+POLICY_ROUTER, POLICY_LRU, POLICY_LFU, POLICY_LRFU = 0, 1, 2, 3
 CTR_A, CTR_HITS, CTR_D, CTR_P, CTR_T = range(NCTR)
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
@@ -29,12 +31,13 @@ _f64p = ctypes.POINTER(ctypes.c_double)
 
 
 class _Cfg(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("L", "N", "K", "C", "R", "S", "mode", "warmup_tokens")]
+    _fields_ = [(n, ctypes.c_int32) for n in ("L", "N", "K", "C", "R", "S", "mode", "warmup_tokens", "policy")] + \
+        [("lrfu_w", ctypes.c_float)]
 
 
 class _State(ctypes.Structure):
     _fields_ = [("cache", _u8p), ("aT", _f32p), ("pS", _f32p), ("ctr", _i64p), ("slot_of", _i32p),
-                ("phys", _i64p), ("n_slots", ctypes.c_int32), ("t", ctypes.c_int32)]
+                ("phys", _i64p), ("pol", _f32p), ("n_slots", ctypes.c_int32), ("t", ctypes.c_int32)]
 
 
 class _Out(ctypes.Structure):
@@ -64,6 +67,8 @@ def lib():
         L.orc_moe_ffn.argtypes = [_f32p, _f32p, _f32p, _f64p, ctypes.c_int, _f32p, ctypes.c_int,
                                   ctypes.c_int, _f64p]
         L.orc_metrics.argtypes = [ctypes.c_int64] * 4 + [ctypes.c_double, _f64p]
+        L.orc_lrfu_weight.argtypes = [ctypes.c_float]
+        L.orc_lrfu_weight.restype = ctypes.c_float
         L.orc_step.argtypes = [ctypes.POINTER(_Cfg), ctypes.POINTER(_State), _f32p, _f32p, _f32p,
                                ctypes.POINTER(_Out)]
         L.orc_step.restype = ctypes.c_int
@@ -163,12 +168,23 @@ def metrics(A: int, D: int, P: int, T: int, expert_bytes: float):
 
 
 # ---------------------------------------------------------------- replay
-class Run:
-    """State of all S streams; ``step`` advances one decode token."""
+def lrfu_weight(lam: float) -> float:
+    """LRFU decay per token, fl32(2^-lambda)."""
+    return float(lib().orc_lrfu_weight(float(lam)))
 
-    def __init__(self, L, N, K, C, R, S, mode, warmup_tokens=0):
-        self.cfg = _Cfg(L, N, K, C, R, S, mode, warmup_tokens)
+
+class Run:
+    """State of all S streams; ``step`` advances one decode token.
+
+    mode: MODE_TEMPORAL (update-only), MODE_SPATIO_TEMPORAL (full) or
+    MODE_SPATIO_ONLY; policy: POLICY_ROUTER (s^T) or a classical retention
+    priority (LRU, LFU, LRFU with ``lrfu_lambda``)."""
+
+    def __init__(self, L, N, K, C, R, S, mode, warmup_tokens=0, policy=POLICY_ROUTER, lrfu_lambda=0.5):
+        self.cfg = _Cfg(L, N, K, C, R, S, mode, warmup_tokens, policy, lrfu_weight(lrfu_lambda))
         self.L, self.N, self.K, self.C, self.S, self.mode = L, N, K, C, S, mode
+        self.policy = policy
+        self.pol = np.zeros((S, L, N), dtype=np.float32)
         self.cache = np.zeros((S, L, N), dtype=np.uint8)
         self.aT = np.zeros((S, L, N), dtype=np.float32)
         self.pS = np.zeros((S, N), dtype=np.float32)
@@ -187,16 +203,20 @@ class Run:
 
     def _state(self):
         return _State(_p(self.cache, _u8p), _p(self.aT, _f32p), _p(self.pS, _f32p), _p(self.ctr, _i64p),
-                      _p(self.slot_of, _i32p), _p(self.phys, _i64p), self.n_slots, self.t)
+                      _p(self.slot_of, _i32p), _p(self.phys, _i64p), _p(self.pol, _f32p), self.n_slots, self.t)
 
-    def step(self, zR, zT, zS=None, want=("sel", "gate")):
-        """zR, zT, zS: [S][L][N] float32.  Returns a dict of per-token outputs."""
+    def step(self, zR, zT=None, zS=None, want=("sel", "gate")):
+        """zR, zT, zS: [S][L][N] float32 (zT only for the router policy in the
+        Temporal / Spatio-Temporal modes, zS only in modes with a Spatio
+        Router).  Returns a dict of per-token outputs."""
         S, L, N, K = self.S, self.L, self.N, self.K
         zR = np.ascontiguousarray(zR, dtype=np.float32).reshape(S, L, N)
-        zT = np.ascontiguousarray(zT, dtype=np.float32).reshape(S, L, N)
+        if self.policy == POLICY_ROUTER and zT is None:
+            raise ValueError("the router policy needs Temporal Router logits")
+        if self.mode in (MODE_SPATIO_TEMPORAL, MODE_SPATIO_ONLY) and zS is None:
+            raise ValueError("this mode needs Spatio Router logits")
+        zT = zR if zT is None else np.ascontiguousarray(zT, dtype=np.float32).reshape(S, L, N)
         zSa = zR if zS is None else np.ascontiguousarray(zS, dtype=np.float32).reshape(S, L, N)
-        if self.mode == 1 and zS is None:
-            raise ValueError("full mode needs Spatio Router logits")
         res = {
             "sel": np.zeros((S, L, K), np.int32), "gate": np.zeros((S, L, K), np.float64),
             "pR": np.zeros((S, L, N), np.float32), "sT": np.zeros((S, L, N), np.float32),

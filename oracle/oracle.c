@@ -15,6 +15,15 @@
  *     Section 3.3 last paragraph, Appendix B.2)
  *   - accounting A, D, P, T and Hit, AdjHit, Load/token           (Section 4.1
  *     "Metrics")
+ *   - the classical cache-update baselines LRU, LFU and LRFU (Section 4.1
+ *     baselines, Table 1 "Cache-Update Methods", LRFU with lambda = 0.5),
+ *     written from their textbook definitions (Mattson et al. 1970 for
+ *     recency; frequency counts; Lee et al. 2001 for the combined
+ *     recency-frequency value with weighing function (1/2)^(lambda x)), as
+ *     the retention priority of the same post-access update (Algorithm 1)
+ *   - the Spatio-only ablation (Section 5 ablations, Appendix B.4):
+ *     s^S = p^R_{t-1,l} + p^S_rho drives the pre-access refinement, and
+ *     demand-miss insertion evicts by LRU
  *   - SwiGLU expert FFN on the selected experts ("execute the MoE layer",
  *     Algorithm 2), in fp64.
  *
@@ -34,6 +43,15 @@
  *     caches in numbered slots; a newly needed expert takes the lowest free
  *     slot, in ascending expert order.  Refinement and the post-access update
  *     each end with such a residency event.
+ *   - Classical priorities live per (stream, layer, expert) and are updated
+ *     once per access, before the eviction decision: LRU stores the time of
+ *     the last use (0 = never), LFU the number of selections, LRFU
+ *     C <- fl32(C * w) (+ 1 if selected), w = fl32(2^-lambda), for every
+ *     expert.  LRU time counts two events per token t: the pre-access
+ *     refinement at 2t + 1 and the access at 2t + 2.  An expert inserted
+ *     proactively (Spatio-only mode) takes time 2t + 1, i.e. enters as the
+ *     most recently used, behind the experts selected at the access that
+ *     follows; frequency policies do not count an insertion as a use.
  *
  * Build: gcc -O2 -ffp-contract=off (no fused multiply-add contraction, no
  * fast-math); fmaf/rintf/ldexpf are the C library's correctly rounded ones.
@@ -265,19 +283,26 @@ void orc_metrics(int64_t A, int64_t D, int64_t P, int64_t T, double expert_bytes
 /* ------------------------------------------------------------------ */
 /* One decode token for all streams                                    */
 /* ------------------------------------------------------------------ */
+enum { ORC_MODE_TEMPORAL = 0, ORC_MODE_SPATIO_TEMPORAL = 1, ORC_MODE_SPATIO_ONLY = 2 };
+enum { ORC_POLICY_ROUTER = 0, ORC_POLICY_LRU = 1, ORC_POLICY_LFU = 2, ORC_POLICY_LRFU = 3 };
+
 typedef struct {
     int32_t L, N, K, C, R, S, mode, warmup_tokens;
+    int32_t policy;   /* retention priority of Algorithm 1: s^T or a classical one */
+    float lrfu_w;     /* LRFU decay per token, fl32(2^-lambda)                    */
 } orc_cfg;
 
 enum { ORC_CTR_A = 0, ORC_CTR_HITS, ORC_CTR_D, ORC_CTR_P, ORC_CTR_T, ORC_NCTR };
 
 typedef struct {
     uint8_t* cache;   /* [S][L][N] logical cache membership                    */
-    float* aT;        /* [S][L][N] s^T of the previous token (full mode)       */
+    float* aT;        /* [S][L][N] previous token's a-score: s^T (full mode),
+                                    p^R (Spatio-only mode)                     */
     float* pS;        /* [S][N]    latest Spatio Router distribution           */
     int64_t* ctr;     /* [S][L][5] A, hits, D, P, T (counted tokens only)       */
     int32_t* slot_of; /* [L][N]    physical slot of each expert, -1 = absent   */
     int64_t* phys;    /* [L][2]    physical fills: demand, proactive (counted)  */
+    float* pol;       /* [S][L][N] classical retention priority (policy != 0)  */
     int32_t n_slots;  /* physical slots per layer                              */
     int32_t t;        /* index of the next token                               */
 } orc_state;
@@ -286,7 +311,7 @@ typedef struct {      /* optional per-token outputs (any pointer may be NULL) */
     int32_t* sel;     /* [S][L][K] selected experts, descending native logit   */
     double* gate;     /* [S][L][K] renormalised selected probabilities         */
     float* pR;        /* [S][L][N] */
-    float* sT;        /* [S][L][N] */
+    float* sT;        /* [S][L][N] retention priority used by Algorithm 1      */
     float* sST;       /* [S][L][N] (full mode, t >= 1)                          */
     int32_t* hits;    /* [S][L] */
     int32_t* nD;      /* [S][L] */
@@ -326,13 +351,35 @@ static int orc_residency(const orc_cfg* c, orc_state* st, int l) {
     return fills;
 }
 
+/* LRFU decay per token: the weighing function (1/2)^(lambda x) at x = 1,
+ * rounded once to fp32. */
+float orc_lrfu_weight(float lambda) { return (float)pow(2.0, -(double)lambda); }
+
+/* Classical retention priority of one (stream, layer) at an access of token
+ * t: the selected experts are used now. */
+static void orc_policy_access(int policy, float w, float* pol, int N, const uint8_t* selected, int t) {
+    for (int e = 0; e < N; ++e) {
+        if (policy == ORC_POLICY_LRU) {
+            if (selected[e]) pol[e] = (float)(2 * t + 2);
+        } else if (policy == ORC_POLICY_LFU) {
+            if (selected[e]) pol[e] = pol[e] + 1.0f;
+        } else if (policy == ORC_POLICY_LRFU) {
+            float v = pol[e] * w;
+            if (selected[e]) v = v + 1.0f;
+            pol[e] = v;
+        }
+    }
+}
+
 /* zR, zT, zS: [S][L][N] fp32 logits of this token (zR already includes any
- * bias; zS ignored in update-only mode).  Returns 0, or -1 on a broken
- * invariant. */
+ * bias; zT is read only with the router policy in the Temporal and
+ * Spatio-Temporal modes, zS only in the modes with a Spatio Router).
+ * Returns 0, or -1 on a broken invariant. */
 int orc_step(const orc_cfg* c, orc_state* st, const float* zR, const float* zT, const float* zS,
              orc_out* out) {
     const int L = c->L, N = c->N, K = c->K, S = c->S;
-    const int full = c->mode == 1;
+    const int spatio = c->mode == ORC_MODE_SPATIO_TEMPORAL || c->mode == ORC_MODE_SPATIO_ONLY;
+    const int router_policy = c->policy == ORC_POLICY_ROUTER;
     const int t = st->t;
     const int counted = t >= c->warmup_tokens;
     float pR[ORC_NMAX], pT[ORC_NMAX], pSn[ORC_NMAX], sT[ORC_NMAX], sST[ORC_NMAX];
@@ -340,13 +387,18 @@ int orc_step(const orc_cfg* c, orc_state* st, const float* zR, const float* zT, 
     for (int l = 0; l < L; ++l) {
         /* Pre-access refinement (Algorithm 2): needs the previous token's
          * same-layer scores, so it starts at t = 1. */
-        if (full && t >= 1 && c->R > 0) {
+        if (spatio && t >= 1 && c->R > 0) {
             for (int s = 0; s < S; ++s) {
                 const size_t sl = (size_t)s * L + l;
-                const float* aT = st->aT + sl * N;       /* p^R_{t-1,l} + p^T_{t-1,l} */
+                /* p^R_{t-1,l} + p^T_{t-1,l} (Spatio-Temporal) or p^R_{t-1,l}
+                 * (Spatio-only) */
+                const float* aT = st->aT + sl * N;
                 const float* pred = st->pS + (size_t)s * N; /* p^S at rho(t,l) */
                 for (int e = 0; e < N; ++e) sST[e] = aT[e] + pred[e];
-                int nP = orc_refine(st->cache + sl * N, N, c->C, sST, c->R, NULL);
+                int32_t loaded[ORC_NMAX];
+                int nP = orc_refine(st->cache + sl * N, N, c->C, sST, c->R, loaded);
+                if (c->policy == ORC_POLICY_LRU)   /* inserted as the most recently used */
+                    for (int i = 0; i < nP; ++i) st->pol[sl * N + loaded[i]] = (float)(2 * t + 1);
                 if (counted) st->ctr[sl * ORC_NCTR + ORC_CTR_P] += nP;
                 if (out && out->nP) out->nP[sl] = nP;
                 if (out && out->sST) memcpy(out->sST + sl * N, sST, sizeof(float) * (size_t)N);
@@ -365,19 +417,28 @@ int orc_step(const orc_cfg* c, orc_state* st, const float* zR, const float* zT, 
         for (int s = 0; s < S; ++s) {
             const size_t sl = (size_t)s * L + l;
             orc_softmax(zR + sl * N, N, pR);
-            orc_softmax(zT + sl * N, N, pT);
             orc_topk(zR + sl * N, N, K, sel);
             double gsum = 0.0;
             for (int k = 0; k < K; ++k) gsum += (double)pR[sel[k]];
-            for (int e = 0; e < N; ++e) sT[e] = pR[e] + pT[e];
+            if (router_policy) {
+                orc_softmax(zT + sl * N, N, pT);
+                for (int e = 0; e < N; ++e) sT[e] = pR[e] + pT[e];
+            } else {
+                uint8_t selected[ORC_NMAX];
+                memset(selected, 0, (size_t)N);
+                for (int k = 0; k < K; ++k) selected[sel[k]] = 1;
+                orc_policy_access(c->policy, c->lrfu_w, st->pol + sl * N, N, selected, t);
+                memcpy(sT, st->pol + sl * N, sizeof(float) * (size_t)N);
+            }
             uint8_t* cache = st->cache + sl * N;
             int hits = 0;
             for (int k = 0; k < K; ++k) hits += cache[sel[k]] ? 1 : 0;
             int nD = orc_update_cache(cache, N, c->C, sel, K, sT, NULL);
             if (hits + nD != K) return -1;
             if (orc_count(cache, N) > c->C) return -1;
-            if (full) {
-                memcpy(st->aT + sl * N, sT, sizeof(float) * (size_t)N);
+            if (spatio) {
+                /* the next token's a-score for this layer */
+                memcpy(st->aT + sl * N, c->mode == ORC_MODE_SPATIO_ONLY ? pR : sT, sizeof(float) * (size_t)N);
                 orc_softmax(zS + sl * N, N, pSn);
                 memcpy(st->pS + (size_t)s * N, pSn, sizeof(float) * (size_t)N);
             }
