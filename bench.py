@@ -27,11 +27,11 @@ HBM_PEAK_GBS = 8000.0
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "ffn_up_bf16_qwen3_30b_traffic.md")
 
 
-def measured_traffic(workload_name):
+def measured_traffic(w):
     """HBM bytes per ffn_up launch from the committed rocprofv3 counter runs,
     or None if they were taken on another workload or on other kernel sources."""
     import hashlib
-    if workload_name != "qwen3_30b" or not os.path.exists(TRAFFIC_PROFILE):
+    if (w.name, w.mode, w.policy, w.C, w.R) != ("qwen3_30b", 0, 0, 32, 0) or not os.path.exists(TRAFFIC_PROFILE):
         return None
     vals = {}
     for line in open(TRAFFIC_PROFILE):
@@ -47,8 +47,14 @@ def measured_traffic(workload_name):
 METRIC = "cache-aware MoE decode token-layer steps/s per GPU; % HBM roofline; hit rate"
 
 
+POLICIES = {"router": 0, "lru": 1, "lfu": 2, "lrfu": 3}
+MODES = {"temporal": 0, "full": 1, "spatio_only": 2}
+
+
 def describe(w):
-    mode = "update-only Temporal Router" if w.mode == 0 else f"full Spatio-Temporal, R={w.R}"
+    retention = {0: "Temporal Router", 1: "LRU", 2: "LFU", 3: f"LRFU(lambda={w.lrfu_lambda})"}[w.policy]
+    mode = {0: f"update-only, {retention} retention", 1: f"full Spatio-Temporal, R={w.R}",
+            2: f"Spatio-only, R={w.R}, {retention} retention"}[w.mode]
     dt = "bf16" if w.dtype == 1 else "fp32"
     return (f"{w.name}: L={w.L} N={w.N} K={w.K} d={w.d} SwiGLU {w.d}->{w.F}->{w.d} C={w.C} {mode}, "
             f"{w.S} streams x {w.T} tokens, {dt}, AR(1) rho={w.rho}"
@@ -61,27 +67,24 @@ def cpu_baseline(w, budget_s):
 
     import oracle
     import synth
-    full = w.mode == 1
-    WR = [synth.router_host(w, synth.KIND_ROUTER_NATIVE, l) for l in range(w.L)]
-    WT = [synth.router_host(w, synth.KIND_ROUTER_TEMPORAL, l) for l in range(w.L)]
-    WS = [synth.router_host(w, synth.KIND_ROUTER_SPATIO, l) for l in range(w.L)] if full else None
+    kinds = [synth.KIND_ROUTER_NATIVE] + ([synth.KIND_ROUTER_TEMPORAL] if w.has_temporal else []) + \
+        ([synth.KIND_ROUTER_SPATIO] if w.has_spatio else [])
+    Ws = [[synth.router_host(w, k, l) for l in range(w.L)] for k in kinds]
     bias = synth.zipf_bias(w)
     Tmax = 64
     H = [synth.hidden_host(w, 0, l, T=Tmax) for l in range(w.L)]
     experts = {}
-    run = oracle.Run(w.L, w.N, w.K, w.C, w.R, 1, w.mode)
+    run = oracle.Run(w.L, w.N, w.K, w.C, w.R, 1, w.mode, policy=w.policy, lrfu_lambda=w.lrfu_lambda)
     busy = 0.0
     tokens = 0
     while tokens < Tmax and (tokens == 0 or busy < budget_s):
         t = tokens
         t0 = time.perf_counter()
-        z = np.empty((3, 1, w.L, w.N), np.float32)
+        z = np.empty((len(kinds), 1, w.L, w.N), np.float32)
         for l in range(w.L):
-            z[0, 0, l] = oracle.logits(WR[l], H[l][t], None if bias is None else bias[l])
-            z[1, 0, l] = oracle.logits(WT[l], H[l][t])
-            if full:
-                z[2, 0, l] = oracle.logits(WS[l], H[l][t])
-        out = run.step(z[0], z[1], z[2] if full else None)
+            for r in range(len(kinds)):
+                z[r, 0, l] = oracle.logits(Ws[r][l], H[l][t], bias[l] if (r == 0 and bias is not None) else None)
+        out = run.step(z[0], z[1] if w.has_temporal else None, z[-1] if w.has_spatio else None)
         busy += time.perf_counter() - t0
         for l in range(w.L):
             sel = out["sel"][0, l]
@@ -107,6 +110,10 @@ def main():
     ap.add_argument("--workload", default="qwen3_30b")
     ap.add_argument("--C", type=int, default=None)
     ap.add_argument("--R", type=int, default=None)
+    ap.add_argument("--policy", choices=sorted(POLICIES), default=None,
+                    help="retention priority (default: the workload's, the Temporal Router)")
+    ap.add_argument("--mode", choices=sorted(MODES), default=None, help="default: the workload's mode")
+    ap.add_argument("--lrfu-lambda", type=float, default=None)
     ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
     ap.add_argument("--no-profile", action="store_true", help="no per-kernel HIP events in the timed region")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
@@ -129,6 +136,12 @@ def main():
     w = synth.WORKLOADS[args.workload]
     if args.C is not None or args.R is not None:
         w = w.replace(C=w.C if args.C is None else args.C, R=w.R if args.R is None else args.R)
+    if args.policy is not None:
+        w = w.replace(policy=POLICIES[args.policy])
+    if args.mode is not None:
+        w = w.replace(mode=MODES[args.mode])
+    if args.lrfu_lambda is not None:
+        w = w.replace(lrfu_lambda=args.lrfu_lambda)
     warmup = args.warmup
     steps = args.steps if args.steps is not None else max(1, w.T - warmup)
     T_gen = min(w.T, warmup + steps)
@@ -183,8 +196,9 @@ def main():
         "dtype": "bf16" if w.dtype == 1 else "f32",
         "data": "synthetic",
         "config": {"workload": describe(w), "streams": w.S, "layers": w.L, "experts": w.N, "top_k": w.K,
-                   "capacity": w.C, "refine_budget": w.R if w.mode == 1 else 0,
-                   "mode": "update-only" if w.mode == 0 else "spatio-temporal", "d": w.d, "F": w.F,
+                   "capacity": w.C, "refine_budget": w.R if w.has_spatio else 0,
+                   "mode": {0: "update-only", 1: "spatio-temporal", 2: "spatio-only"}[w.mode],
+                   "retention": {v: k for k, v in POLICIES.items()}[w.policy], "d": w.d, "F": w.F,
                    "fills": "main stream" if args.fill_on_main else "side stream"},
     }
     # algorithmic bytes of one token step: each distinct selected expert read
@@ -202,7 +216,7 @@ def main():
         gbs = bytes_up / avg_s / 1e9
         res["roofline"] = {"kernel": "ffn_up_bf16" if w.dtype == 1 else "ffn_up_f32", "bound": "hbm",
                            "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
-                           "traffic": measured_traffic(w.name), "avg_launch_us": avg_s * 1e6, "algorithmic_bytes_per_launch": bytes_up}
+                           "traffic": measured_traffic(w), "avg_launch_us": avg_s * 1e6, "algorithmic_bytes_per_launch": bytes_up}
 
     A, D, P, Tc = tot["accesses"], tot["demand_misses"], tot["proactive_loads"], tot["tokens"]
     res["cache"] = {"hit": 1 - D / A, "adj_hit": (A - D) / (A + P), "load_mb_per_token": (D + P) * w.expert_bytes

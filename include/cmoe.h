@@ -10,6 +10,12 @@
  *                                                                         Algorithm 2)
  *   - the post-access retention update U_C of each per-(stream, layer)
  *     cache of capacity C                                                (Algorithm 1)
+ *     with the Temporal Router's s^T as priority, or one of the classical
+ *     cache-update baselines LRU, LFU, LRFU                              (Section 4.1,
+ *                                                                         Table 1)
+ *   - the Spatio-only ablation: refinement over Top_R(p^R_{t-1} + p^S)
+ *     with classical eviction of demand misses                           (Section 5,
+ *                                                                         Appendix B.4)
  *   - the accounting of accesses A, hits, demand misses D, proactive
  *     loads P, decode tokens T and expert-weight traffic (D + P) S_exp    (Section 4.1)
  *   - copies of newly needed experts from a cold pool into HBM slots
@@ -49,9 +55,30 @@ typedef enum {
 } cmoe_status;
 
 typedef enum {
-    CMOE_MODE_TEMPORAL = 0,        /* update-only Temporal Router (Section 3.2)   */
-    CMOE_MODE_SPATIO_TEMPORAL = 1  /* full mode with refinement (Section 3.3)     */
+    CMOE_MODE_TEMPORAL = 0,         /* update-only: no refinement (Section 3.2)    */
+    CMOE_MODE_SPATIO_TEMPORAL = 1,  /* full mode with refinement (Section 3.3)     */
+    CMOE_MODE_SPATIO_ONLY = 2       /* refinement by p^R_{t-1} + p^S, classical
+                                       retention (Section 5, Appendix B.4)         */
 } cmoe_mode;
+
+/* Retention priority of the post-access update (Algorithm 1): the selected
+ * experts are protected and, when the cache is full, each demand-loaded
+ * expert replaces the lowest-priority resident that is not selected now
+ * (lower expert index on ties).  The classical priorities follow their
+ * textbook definitions and are updated at every access before the eviction:
+ *   LRU   time of the last use (two events per token t: refinement at 2t + 1,
+ *         access at 2t + 2; a proactively inserted expert takes 2t + 1);
+ *   LFU   number of selections;
+ *   LRFU  C <- fl32(C * w) (+ 1 if selected) for every expert,
+ *         w = fl32(2^-lrfu_lambda) (Lee et al. 2001).
+ * They use the native router only.  CMOE_MODE_SPATIO_TEMPORAL needs
+ * CMOE_POLICY_ROUTER; CMOE_MODE_SPATIO_ONLY needs a classical policy. */
+typedef enum {
+    CMOE_POLICY_ROUTER = 0,  /* s^T = p^R + p^T of the Temporal Router           */
+    CMOE_POLICY_LRU = 1,
+    CMOE_POLICY_LFU = 2,
+    CMOE_POLICY_LRFU = 3
+} cmoe_policy;
 
 typedef enum {
     CMOE_F32 = 0,  /* fp32 weights and hidden states                          */
@@ -69,8 +96,10 @@ typedef enum {
                                        the layer's FFN)                          */
 
 /* Problem shape.  Valid values: 1 <= K <= C <= N (Section 2: capacity at least
- * Top-K); 0 <= R <= N; L, S >= 1; d, F >= 1; warmup_tokens >= 0.  Supported:
- * N <= 256, d and F multiples of 64.  R is ignored in CMOE_MODE_TEMPORAL. */
+ * Top-K); 0 <= R <= N; L, S >= 1; d, F >= 1; warmup_tokens >= 0; a known mode
+ * and policy, paired as cmoe_policy states; lrfu_lambda finite and >= 0 with
+ * CMOE_POLICY_LRFU.  Supported: N <= 256, d and F multiples of 64.  R is
+ * ignored in CMOE_MODE_TEMPORAL. */
 typedef struct {
     int32_t L, N, K, d, F, C, R, S;
     int32_t mode;          /* cmoe_mode                                         */
@@ -79,6 +108,8 @@ typedef struct {
     int32_t warmup_tokens; /* leading tokens whose transfers are not counted
                               (the paper excludes prefill transfers)            */
     uint32_t flags;
+    int32_t policy;        /* cmoe_policy                                       */
+    float lrfu_lambda;     /* LRFU recency weight (the paper uses 0.5)          */
 } cmoe_config;
 
 /* Weights (device pointers unless stated).  Router matrices are bias-free
@@ -89,8 +120,10 @@ typedef struct {
  * the device (hipHostMalloc). */
 typedef struct {
     const void* w_router;    /* W^R [L][N][d]                                    */
-    const void* w_temporal;  /* W^T [L][N][d]                                    */
-    const void* w_spatio;    /* W^S [L][N][d]; required in full mode, else NULL  */
+    const void* w_temporal;  /* W^T [L][N][d]; required with CMOE_POLICY_ROUTER,
+                                else ignored                                     */
+    const void* w_spatio;    /* W^S [L][N][d]; required in the two modes with a
+                                Spatio Router, else ignored                      */
     const float* logit_bias; /* [L][N] fp32 added to native logits, or NULL      */
     const void* cold_pool;   /* [L][N][expert_bytes]                             */
 } cmoe_weights;
@@ -137,7 +170,8 @@ cmoe_status cmoe_step(cmoe_handle* hd, const void* h, float* y);
 /* The cache path of one token from given fp32 logits, without the router
  * GEMV and without the FFN: softmax, Top-K, refinement, access, retention,
  * counters, residency and fills.  zR (native, bias already added), zT, zS:
- * [S][L][N] fp32 (device); zS is ignored in update-only mode. */
+ * [S][L][N] fp32 (device); zT is required with CMOE_POLICY_ROUTER and zS in
+ * the modes with a Spatio Router; otherwise they are ignored (may be NULL). */
 cmoe_status cmoe_step_logits(cmoe_handle* hd, const float* zR, const float* zT, const float* zS);
 
 /* Synchronizes both streams and reads the counters.  total may be NULL.
@@ -169,8 +203,9 @@ cmoe_status cmoe_reset(cmoe_handle* hd);
 cmoe_status cmoe_destroy(cmoe_handle* hd);
 
 /* Inspectable state (all synchronize).  Layouts:
- *   CMOE_VIEW_LOGITS    fp32  [L][S][n_r][N] logits used by the last token,
- *                              n_r = 2 (native, temporal) or 3 (+ spatio)
+ *   CMOE_VIEW_LOGITS    fp32  [L][S][n_r][N] logits used by the last token:
+ *                              native, then temporal (router policy), then
+ *                              spatio (modes with a Spatio Router)
  *   CMOE_VIEW_SELECTED  int32 [L][S][K] selected experts, descending logit
  *   CMOE_VIEW_GATES     fp32  [L][S][K] renormalised selected probabilities
  *   CMOE_VIEW_CACHE     u64   [S][L][W] cache membership bit masks,
@@ -181,7 +216,9 @@ cmoe_status cmoe_destroy(cmoe_handle* hd);
  *   CMOE_VIEW_EVENTS    int32 [L][S][4] last token: hits, D, P, 0
  *   CMOE_VIEW_FILLS     int32 [L][2] last token's physical fills: demand, proactive
  *   CMOE_VIEW_ACTIVE    int64 [L] distinct experts executed by the FFN, summed
- *                              over counted tokens (each is one read of its weights) */
+ *                              over counted tokens (each is one read of its weights)
+ *   CMOE_VIEW_PRIORITY  fp32  [S][L][N] classical retention priority (LRU time,
+ *                              LFU count, LRFU value); zeros with the router policy */
 enum {
     CMOE_VIEW_LOGITS = 0,
     CMOE_VIEW_SELECTED = 1,
@@ -193,7 +230,8 @@ enum {
     CMOE_VIEW_EVENTS = 7,
     CMOE_VIEW_FILLS = 8,
     CMOE_VIEW_ACTIVE = 9,
-    CMOE_VIEW_COUNT = 10
+    CMOE_VIEW_PRIORITY = 10,
+    CMOE_VIEW_COUNT = 11
 };
 
 /* Bytes of a view (0 for an unknown view or a NULL handle). */

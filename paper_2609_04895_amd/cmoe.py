@@ -24,6 +24,11 @@ CMOE_ERR_STATE = -4
 
 CMOE_MODE_TEMPORAL = 0
 CMOE_MODE_SPATIO_TEMPORAL = 1
+CMOE_MODE_SPATIO_ONLY = 2
+CMOE_POLICY_ROUTER = 0
+CMOE_POLICY_LRU = 1
+CMOE_POLICY_LFU = 2
+CMOE_POLICY_LRFU = 3
 CMOE_F32 = 0
 CMOE_BF16 = 1
 CMOE_POOL_DEVICE = 0
@@ -40,6 +45,7 @@ CMOE_VIEW_SLOTS = 6
 CMOE_VIEW_EVENTS = 7
 CMOE_VIEW_FILLS = 8
 CMOE_VIEW_ACTIVE = 9
+CMOE_VIEW_PRIORITY = 10
 CMOE_KERNEL_COUNT = 6
 KERNEL_NAMES = ("router", "cache_step", "fill", "ffn_up", "ffn_down", "combine")
 
@@ -50,7 +56,8 @@ EXPORTED = ("cmoe_query", "cmoe_init", "cmoe_step", "cmoe_step_logits", "cmoe_st
 
 class cmoe_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("L", "N", "K", "d", "F", "C", "R", "S", "mode", "dtype",
-                                              "pool_kind", "warmup_tokens")] + [("flags", ctypes.c_uint32)]
+                                              "pool_kind", "warmup_tokens")] + \
+        [("flags", ctypes.c_uint32), ("policy", ctypes.c_int32), ("lrfu_lambda", ctypes.c_float)]
 
 
 class cmoe_weights(ctypes.Structure):
@@ -122,8 +129,19 @@ def _check(status: int):
         raise CmoeError(status, lib().cmoe_last_error().decode())
 
 
-def make_config(L, N, K, d, F, C, R, S, mode, dtype, pool_kind=CMOE_POOL_DEVICE, warmup_tokens=0, flags=0):
-    return cmoe_config(L, N, K, d, F, C, R, S, mode, dtype, pool_kind, warmup_tokens, flags)
+def make_config(L, N, K, d, F, C, R, S, mode, dtype, pool_kind=CMOE_POOL_DEVICE, warmup_tokens=0, flags=0,
+                policy=CMOE_POLICY_ROUTER, lrfu_lambda=0.5):
+    return cmoe_config(L, N, K, d, F, C, R, S, mode, dtype, pool_kind, warmup_tokens, flags, policy, lrfu_lambda)
+
+
+def router_slots(cfg: cmoe_config):
+    """Names of the router slots of the logits view, in order."""
+    names = ["native"]
+    if cfg.policy == CMOE_POLICY_ROUTER:
+        names.append("temporal")
+    if cfg.mode in (CMOE_MODE_SPATIO_TEMPORAL, CMOE_MODE_SPATIO_ONLY):
+        names.append("spatio")
+    return names
 
 
 def cmoe_query(cfg: cmoe_config) -> cmoe_sizes:
@@ -170,8 +188,8 @@ class Engine:
     def cmoe_step(self, h, y):
         _check(lib().cmoe_step(self.handle, ctypes.c_void_p(h.data_ptr()), ctypes.c_void_p(y.data_ptr())))
 
-    def cmoe_step_logits(self, zR, zT, zS=None):
-        _check(lib().cmoe_step_logits(self.handle, ctypes.c_void_p(zR.data_ptr()), ctypes.c_void_p(zT.data_ptr()),
+    def cmoe_step_logits(self, zR, zT=None, zS=None):
+        _check(lib().cmoe_step_logits(self.handle, ctypes.c_void_p(zR.data_ptr()), ctypes.c_void_p(_ptr(zT)),
                                       ctypes.c_void_p(_ptr(zS))))
 
     # -- counters and state
@@ -205,7 +223,7 @@ class Engine:
         n = lib().cmoe_view_bytes(self.handle, view)
         raw = np.empty(n, np.uint8)
         _check(lib().cmoe_read(self.handle, view, raw.ctypes.data_as(ctypes.c_void_p), n))
-        n_r = 3 if c.mode == CMOE_MODE_SPATIO_TEMPORAL else 2
+        n_r = len(router_slots(c))
         NW = (c.N + 63) // 64
         shapes = {
             CMOE_VIEW_LOGITS: (np.float32, (c.L, c.S, n_r, c.N)),
@@ -218,6 +236,7 @@ class Engine:
             CMOE_VIEW_EVENTS: (np.int32, (c.L, c.S, 4)),
             CMOE_VIEW_FILLS: (np.int32, (c.L, 2)),
             CMOE_VIEW_ACTIVE: (np.int64, (c.L,)),
+            CMOE_VIEW_PRIORITY: (np.float32, (c.S, c.L, c.N)),
         }
         dt, shape = shapes[view]
         return raw.view(dt).reshape(shape)

@@ -4,22 +4,27 @@
 // lane e % 64, register e / 64.  For the accessed layer l it
 //   - finishes the router logits (adds the split-K partials in ascending
 //     order, adds the native bias, rounds once to fp32),
-//   - computes p^R, p^T (and p^S in full mode) with the fixed fp32 softmax
-//     described below (Section 2, Section 3.2, Section 3.3),
+//   - computes p^R, p^T (router policy) and p^S (modes with a Spatio
+//     Router) with the fixed fp32 softmax described below (Section 2,
+//     Section 3.2, Section 3.3),
 //   - selects S = TopK by native logit (ties: lower index) and the gate
 //     weights p^R_S / sum p^R_S,
 //   - counts hits and demand misses against the resident set (Section 2),
-//   - applies the post-access retention update with s^T = p^R + p^T
-//     (Algorithm 1: each demand-loaded expert in ascending order fills free
-//     room or replaces the lowest-s^T resident that is not selected now;
-//     ties evict the lower index),
-//   - stores s^T as the next token's a^T (Section 3.3) and p^S as the
-//     prediction for the causal successor.
-// In full mode it then refines the successor layer's cache before that
-// layer is accessed (Algorithm 2): candidates Top_R(s^ST), s^ST = a^T + p^S
-// of the causal predecessor, examined in descending order; a non-resident
-// candidate fills free room, else replaces the lowest-s^ST resident when its
-// score is strictly higher.  The first layer of a token is refined by a
+//   - applies the post-access retention update (Algorithm 1: each
+//     demand-loaded expert in ascending order fills free room or replaces
+//     the lowest-priority resident that is not selected now; ties evict the
+//     lower index), with priority s^T = p^R + p^T or, for the classical
+//     cache-update baselines (Section 4.1, Table 1), the LRU time, LFU count
+//     or LRFU value, updated first,
+//   - stores the next token's a-score (Section 3.3: s^T in the full mode;
+//     p^R in the Spatio-only ablation of Section 5 / Appendix B.4) and p^S
+//     as the prediction for the causal successor.
+// In the modes with a Spatio Router it then refines the successor layer's
+// cache before that layer is accessed (Algorithm 2): candidates Top_R(s^ST),
+// s^ST = a + p^S of the causal predecessor, examined in descending order; a
+// non-resident candidate fills free room, else replaces the lowest-s^ST
+// resident when its score is strictly higher (an inserted expert takes the
+// LRU time of the refinement).  The first layer of a token is refined by a
 // refine-only launch at the start of the token, from the previous token's
 // last-layer p^S (the wrap-around of the causal predecessor).
 //
@@ -44,6 +49,8 @@
 namespace cmoe {
 
 namespace {
+
+constexpr int kPolicyRouter = 0, kPolicyLRU = 1, kPolicyLFU = 2;  // cmoe_policy; 3 = LRFU
 
 constexpr float kLn2Hi = 0x1.62e4p-1f;       // 0x3f317200
 constexpr float kLn2Lo = 0x1.7f7d1cp-20f;    // 0x35bfbe8e
@@ -256,7 +263,7 @@ __device__ inline void clear_bit(unsigned long long (&w)[NPL], int e) {
 
 // Pre-access refinement of one (stream, layer) cache (Algorithm 2).
 template <int NPL>
-__device__ void refine_one(const Layout& lo, int s, int rl, int R, bool counted, const float (&pred)[NPL],
+__device__ void refine_one(const Layout& lo, int s, int rl, int R, int t, bool counted, const float (&pred)[NPL],
                            const float (&aTv)[NPL], const unsigned long long (&cw_in)[NPL], int64_t ctr_p, int lane) {
     const int N = lo.N;
     float sST[NPL];
@@ -281,6 +288,9 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, bool counted,
         count += __popcll(cw[j]);
     }
     int nP = 0;
+    unsigned long long ins[NPL];  // experts inserted here
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) ins[j] = 0ull;
     const int Rn = R < N ? R : N;
     for (int i = 0; i < Rn; ++i) {
         unsigned long long best = 0ull;
@@ -295,6 +305,7 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, bool counted,
         if (bit_of(cw, e)) continue;              // already resident
         if (count < lo.C) {
             set_bit(cw, e);
+            set_bit(ins, e);
             ++count;
             ++nP;
         } else {
@@ -303,9 +314,18 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, bool counted,
             const uint32_t ord_v = (uint32_t)(mn >> 32);
             if (ord_e > ord_v) {  // strictly higher priority
                 clear_bit(cw, v);
+                clear_bit(ins, v);
                 set_bit(cw, e);
+                set_bit(ins, e);
                 ++nP;
             }
+        }
+    }
+    if (lo.policy == kPolicyLRU) {  // inserted as the most recently used, at 2t + 1
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+            const int e = j * 64 + lane;
+            if (e < N && ((ins[j] >> lane) & 1ull)) lo.pol[((int64_t)s * lo.L + rl) * N + e] = (float)(2 * t + 1);
         }
     }
     if (lane == 0) {
@@ -318,7 +338,8 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, bool counted,
 template <int NPL, int NR, bool INJECT, int ZS>
 __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane) {
     const int N = lo.N, L = lo.L, K = lo.K;
-    const bool full = lo.mode == 1;
+    const bool spatio = lo.iS > 0;           // a Spatio Router: stores a-score and p^S
+    const bool classical = lo.policy != kPolicyRouter;
     const bool counted = (a.flags & kFlagCount) != 0;
     float pred[NPL];
 
@@ -337,12 +358,14 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
         }
         if (refine) ctr_rp = lo.ctr[((int64_t)s * L + a.rl) * kNctr + kCtrP];
     }
+    float polv[NPL];  // classical priority of the accessed layer
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
         const int e = j * 64 + lane;
         aTv[j] = (refine && e < N) ? lo.aT[((int64_t)s * L + a.rl) * N + e] : 0.0f;
         cw_r[j] = (refine && j < lo.NW) ? lo.cache[((int64_t)s * L + a.rl) * lo.NW + j] : 0ull;
         cw_a[j] = ((a.flags & kFlagAccess) && j < lo.NW) ? lo.cache[((int64_t)s * L + a.l) * lo.NW + j] : 0ull;
+        polv[j] = (classical && (a.flags & kFlagAccess) && e < N) ? lo.pol[((int64_t)s * L + a.l) * N + e] : 0.0f;
     }
 
     if (a.flags & kFlagAccess) {
@@ -363,8 +386,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
 #pragma unroll
             for (int r = 0; r < NR; ++r) {
                 if (INJECT) {
-                    const float* src = r == 0 ? a.zR : (r == 1 ? a.zT : a.zS);
-                    zin[r][j] = src[sl * N + ec];
+                    zin[r][j] = a.z[r][sl * N + ec];
                 } else {
                     const double2* zp =
                         reinterpret_cast<const double2*>(lo.zpart + (((int64_t)s * NR + r) * N + ec) * ZS);
@@ -375,7 +397,9 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
         }
         float z[3][NPL];
 #pragma unroll
-        for (int j = 0; j < NPL; ++j) z[2][j] = 0.0f;
+        for (int r = NR; r < 3; ++r)
+#pragma unroll
+            for (int j = 0; j < NPL; ++j) z[r][j] = 0.0f;
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
 #pragma unroll
@@ -396,10 +420,11 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
                 z[r][j] = e < N ? v : 0.0f;
             }
         }
+        // router slots: 0 native, then temporal (router policy), then spatio
         float pR[NPL], pT[NPL];
         softmax_fixed<NPL>(z[0], N, lane, pR);
-        softmax_fixed<NPL>(z[1], N, lane, pT);
-        if (full) softmax_fixed<NPL>(z[2], N, lane, pred);
+        if (NR >= 2 && !classical) softmax_fixed<NPL>(z[1], N, lane, pT);
+        if (NR >= 2 && spatio) softmax_fixed<NPL>(z[NR - 1], N, lane, pred);
 
         // Top-K by native logit, lower index first on ties
         unsigned long long key[NPL];
@@ -447,9 +472,29 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             lo.pairs[be * lo.S + pos] = (s << 8) | lane;
             if (pos == 0 && counted) atomicAdd(&lo.active_sum[l], 1ull);
         }
+        // retention priority of Algorithm 1
         float sT[NPL];
+        if (!classical) {
 #pragma unroll
-        for (int j = 0; j < NPL; ++j) sT[j] = pR[j] + pT[j];
+            for (int j = 0; j < NPL; ++j) sT[j] = pR[j] + pT[j];
+        } else {
+#pragma unroll
+            for (int j = 0; j < NPL; ++j) {
+                const bool used = (sw[j] >> lane) & 1ull;
+                float v = polv[j];
+                if (lo.policy == kPolicyLRU) {
+                    if (used) v = (float)(2 * a.t + 2);
+                } else if (lo.policy == kPolicyLFU) {
+                    if (used) v = v + 1.0f;
+                } else {
+                    v = v * lo.lrfu_w;
+                    if (used) v = v + 1.0f;
+                }
+                sT[j] = v;
+                const int e = j * 64 + lane;
+                if (e < N) lo.pol[sl * N + e] = v;
+            }
+        }
 
         // access
         unsigned long long* cptr = lo.cache + sl * lo.NW;
@@ -498,12 +543,13 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
                 c[kCtrT] = ctr_a[kCtrT] + 1;
             }
         }
-        if (full) {
+        if (spatio) {  // the next token's a-score of this layer, and p^S for the successor
+            const bool spatio_only = lo.iT < 0;
 #pragma unroll
             for (int j = 0; j < NPL; ++j) {
                 const int e = j * 64 + lane;
                 if (e < N) {
-                    lo.aT[sl * N + e] = sT[j];
+                    lo.aT[sl * N + e] = spatio_only ? pR[j] : sT[j];
                     lo.pS[(int64_t)s * N + e] = pred[j];
                 }
             }
@@ -516,7 +562,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             pred[j] = e < N ? lo.pS[(int64_t)s * N + e] : 0.0f;
         }
     }
-    if (refine) refine_one<NPL>(lo, s, a.rl, a.R, counted, pred, aTv, cw_r, ctr_rp, lane);
+    if (refine) refine_one<NPL>(lo, s, a.rl, a.R, a.t, counted, pred, aTv, cw_r, ctr_rp, lane);
 }
 
 template <int NPL, int NR, bool INJECT, int ZS>
@@ -538,7 +584,10 @@ __global__ void init_kernel(Layout lo) {
     const int64_t nc = (int64_t)lo.S * lo.L * lo.NW;
     for (int64_t i = gid; i < nc; i += gs) lo.cache[i] = 0ull;
     const int64_t na = (int64_t)lo.S * lo.L * lo.N;
-    for (int64_t i = gid; i < na; i += gs) lo.aT[i] = 0.0f;
+    for (int64_t i = gid; i < na; i += gs) {
+        lo.aT[i] = 0.0f;
+        lo.pol[i] = 0.0f;
+    }
     for (int64_t i = gid; i < (int64_t)lo.S * lo.N; i += gs) lo.pS[i] = 0.0f;
     for (int64_t i = gid; i < (int64_t)lo.S * lo.L * kNctr; i += gs) lo.ctr[i] = 0;
     for (int64_t i = gid; i < (int64_t)lo.L * 2; i += gs) {
@@ -575,7 +624,9 @@ hipError_t launch_step_nr(const Layout& lo, const StepArgs& a, hipStream_t st) {
 
 template <int NPL>
 hipError_t launch_step_npl(const Layout& lo, const StepArgs& a, hipStream_t st) {
-    return lo.n_r == 3 ? launch_step_nr<NPL, 3>(lo, a, st) : launch_step_nr<NPL, 2>(lo, a, st);
+    if (lo.n_r == 3) return launch_step_nr<NPL, 3>(lo, a, st);
+    if (lo.n_r == 2) return launch_step_nr<NPL, 2>(lo, a, st);
+    return launch_step_nr<NPL, 1>(lo, a, st);
 }
 
 hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st) {

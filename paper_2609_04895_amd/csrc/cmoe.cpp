@@ -2,19 +2,21 @@
 // buffer carving, the per-token launch sequence on the main and side streams,
 // counters, inspection and kernel timing.
 //
-// Launch sequence of one token (layers in causal order):
-//   [full mode, t >= 1, R > 0] main: cache step refining layer 0 from the
+// Launch sequence of one token (layers in causal order; "refining modes" are
+// the full and Spatio-only modes, which have a Spatio Router):
+//   [refining mode, t >= 1, R > 0] main: cache step refining layer 0 from the
 //       previous token's last-layer Spatio prediction; side: fill (proactive)
 //   for each layer l:
 //     main: router GEMV(l)
 //     main: [wait for the proactive fill of l] cache step(l): access, retention,
-//           counters, buckets; in full mode also refinement of layer l + 1
+//           counters, buckets; in a refining mode also refinement of layer l + 1
 //     main: fill(l, demand)  -- gates the FFN of this layer
-//     side: [full mode] fill(l + 1, proactive), overlapping the FFN of l
+//     side: [refining mode] fill(l + 1, proactive), overlapping the FFN of l
 //     main: expert gate/up(l), expert down(l), combine(l)
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -42,8 +44,11 @@ enum KernelId { KID_ROUTER = 0, KID_CACHE = 1, KID_FILL = 2, KID_UP = 3, KID_DOW
 
 struct Derived {
     int NW, n_r, n_slots, nsplit, rdk, zstride;
+    int iT, iS;        // router slots of the Temporal / Spatio Router, -1 if not used
     size_t esz, expert_bytes;
 };
+
+bool has_spatio(int mode) { return mode == CMOE_MODE_SPATIO_TEMPORAL || mode == CMOE_MODE_SPATIO_ONLY; }
 
 cmoe_status validate(const cmoe_config* c, Derived* dv) {
     if (!c) return fail(CMOE_ERR_INVALID_ARG, "config is NULL");
@@ -51,8 +56,16 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
         return fail(CMOE_ERR_INVALID_ARG, "L, S, N, K, d and F must be >= 1");
     if (c->K > c->C) return fail(CMOE_ERR_INVALID_ARG, "capacity C must be at least K");
     if (c->C > c->N) return fail(CMOE_ERR_INVALID_ARG, "capacity C must not exceed N");
-    if (c->mode != CMOE_MODE_TEMPORAL && c->mode != CMOE_MODE_SPATIO_TEMPORAL)
+    if (c->mode != CMOE_MODE_TEMPORAL && c->mode != CMOE_MODE_SPATIO_TEMPORAL && c->mode != CMOE_MODE_SPATIO_ONLY)
         return fail(CMOE_ERR_INVALID_ARG, "unknown mode");
+    if (c->policy < CMOE_POLICY_ROUTER || c->policy > CMOE_POLICY_LRFU)
+        return fail(CMOE_ERR_INVALID_ARG, "unknown policy");
+    if (c->mode == CMOE_MODE_SPATIO_ONLY && c->policy == CMOE_POLICY_ROUTER)
+        return fail(CMOE_ERR_INVALID_ARG, "the Spatio-only mode has no Temporal Router: choose LRU, LFU or LRFU");
+    if (c->mode == CMOE_MODE_SPATIO_TEMPORAL && c->policy != CMOE_POLICY_ROUTER)
+        return fail(CMOE_ERR_UNSUPPORTED, "the full mode retains by the Temporal Router's s^T");
+    if (c->policy == CMOE_POLICY_LRFU && !(std::isfinite(c->lrfu_lambda) && c->lrfu_lambda >= 0.0f))
+        return fail(CMOE_ERR_INVALID_ARG, "lrfu_lambda must be finite and >= 0");
     if (c->R < 0 || c->R > c->N) return fail(CMOE_ERR_INVALID_ARG, "R must be in [0, N]");
     if (c->dtype != CMOE_F32 && c->dtype != CMOE_BF16) return fail(CMOE_ERR_INVALID_ARG, "unknown dtype");
     if (c->pool_kind != CMOE_POOL_DEVICE && c->pool_kind != CMOE_POOL_HOST_PINNED)
@@ -63,7 +76,10 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     if (c->d % 64 || c->F % 64) return fail(CMOE_ERR_UNSUPPORTED, "d and F must be multiples of 64");
     if ((int64_t)c->S * c->K >= (int64_t)1 << 23) return fail(CMOE_ERR_UNSUPPORTED, "S*K too large");
     dv->NW = (c->N + 63) / 64;
-    dv->n_r = c->mode == CMOE_MODE_SPATIO_TEMPORAL ? 3 : 2;
+    const bool temporal = c->policy == CMOE_POLICY_ROUTER;
+    dv->iT = temporal ? 1 : -1;
+    dv->iS = has_spatio(c->mode) ? (temporal ? 2 : 1) : -1;
+    dv->n_r = 1 + (temporal ? 1 : 0) + (has_spatio(c->mode) ? 1 : 0);
     dv->n_slots = (int)std::min<int64_t>(c->N, (int64_t)c->S * c->C);
     dv->esz = c->dtype == CMOE_BF16 ? 2 : 4;
     dv->expert_bytes = (size_t)3 * c->d * c->F * dv->esz;
@@ -85,7 +101,7 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
 
 // Offsets of every sub-buffer; used both for sizing and for carving.
 struct Plan {
-    size_t cache, aT, pS, ctr, phys, active_sum, slot_of, slot_exp, state_total;
+    size_t cache, aT, pol, pS, ctr, phys, active_sum, slot_of, slot_exp, state_total;
     size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, zero_row, ws_total;
     size_t arena;
 };
@@ -101,6 +117,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     };
     p.cache = take(S * L * dv.NW * 8);
     p.aT = take(S * L * N * 4);
+    p.pol = take(S * L * N * 4);
     p.pS = take(S * N * 4);
     p.ctr = take(S * L * cmoe::kNctr * 8);
     p.phys = take(L * 2 * 8);
@@ -204,14 +221,13 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
     const cmoe_config& c = hd->cfg;
     const Layout& lo = hd->lo;
     const bool inject = h == nullptr;
-    const bool full = c.mode == CMOE_MODE_SPATIO_TEMPORAL;
-    const bool refine_on = full && hd->t >= 1 && hd->R > 0;
+    const bool refine_on = has_spatio(c.mode) && hd->t >= 1 && hd->R > 0;
     const bool counted = hd->t >= c.warmup_tokens;
     const uint32_t count = counted ? cmoe::kFlagCount : 0u;
     hipStream_t M = hd->main, Sd = hd->side;
 
     if (refine_on) {  // layer 0: refined from the previous token's last-layer prediction
-        StepArgs a{0, 0, hd->R, 0, cmoe::kFlagRefine | count, zR, zT, zS};
+        StepArgs a{0, 0, hd->R, 0, cmoe::kFlagRefine | count, hd->t, {nullptr, nullptr, nullptr}};
         HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "refine layer 0");
         if (!hd->side_is_main) {
             HIPCHK(hipEventRecord(hd->ev_access[0], M), "event record");
@@ -231,7 +247,9 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
         if (refine_on) flags |= cmoe::kFlagRefinedHere;
         if (refine_next) flags |= cmoe::kFlagRefine;
         const int bbuf = (int)(hd->g & 1);
-        StepArgs a{l, l + 1, hd->R, bbuf, flags, zR, zT, zS};
+        StepArgs a{l, l + 1, hd->R, bbuf, flags, hd->t, {zR, nullptr, nullptr}};
+        if (hd->dv.iT > 0) a.z[hd->dv.iT] = zT;
+        if (hd->dv.iS > 0) a.z[hd->dv.iS] = zS;
         HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "cache step");
         hd->g += 1;
         HIPCHK(fill(hd, l, 0, counted, !refine_on, M), "fill");  // demand loads gate this layer's FFN
@@ -286,10 +304,11 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     cmoe_status st = validate(cfg, &dv);
     if (st != CMOE_OK) return st;
     if (!w || !buf || !out) return fail(CMOE_ERR_INVALID_ARG, "weights, buffers and output handle are required");
-    if (!w->w_router || !w->w_temporal || !w->cold_pool)
-        return fail(CMOE_ERR_INVALID_ARG, "w_router, w_temporal and cold_pool are required");
-    if (cfg->mode == CMOE_MODE_SPATIO_TEMPORAL && !w->w_spatio)
-        return fail(CMOE_ERR_INVALID_ARG, "w_spatio is required in full mode");
+    if (!w->w_router || !w->cold_pool) return fail(CMOE_ERR_INVALID_ARG, "w_router and cold_pool are required");
+    if (dv.iT > 0 && !w->w_temporal)
+        return fail(CMOE_ERR_INVALID_ARG, "w_temporal is required with the router policy");
+    if (dv.iS > 0 && !w->w_spatio)
+        return fail(CMOE_ERR_INVALID_ARG, "w_spatio is required in the modes with a Spatio Router");
     if (!buf->arena || !buf->state || !buf->workspace)
         return fail(CMOE_ERR_INVALID_ARG, "arena, state and workspace buffers are required");
     for (const void* p : {buf->arena, buf->state, buf->workspace})
@@ -318,7 +337,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     hd->cfg = *cfg;
     hd->dv = dv;
     hd->plan = make_plan(cfg, dv);
-    hd->R = cfg->mode == CMOE_MODE_SPATIO_TEMPORAL ? cfg->R : 0;
+    hd->R = has_spatio(cfg->mode) ? cfg->R : 0;
     hd->ver.assign(cfg->L, 0);
     hd->main = static_cast<hipStream_t>(main_stream);
     hd->side_is_main = side_stream == nullptr || side_stream == main_stream || (cfg->flags & CMOE_FLAG_FILL_ON_MAIN);
@@ -329,13 +348,19 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.L = cfg->L; lo.N = cfg->N; lo.K = cfg->K; lo.d = cfg->d; lo.F = cfg->F; lo.C = cfg->C; lo.S = cfg->S;
     lo.mode = cfg->mode; lo.dtype = cfg->dtype; lo.NW = dv.NW; lo.n_slots = dv.n_slots; lo.n_r = dv.n_r;
     lo.nsplit = dv.nsplit; lo.rdk = dv.rdk; lo.zstride = dv.zstride; lo.warmup = cfg->warmup_tokens;
+    lo.iT = dv.iT; lo.iS = dv.iS; lo.policy = cfg->policy;
+    lo.lrfu_w = (float)std::pow(2.0, -(double)cfg->lrfu_lambda);
     lo.expert_elems = (int64_t)3 * cfg->d * cfg->F;
-    lo.wR = w->w_router; lo.wT = w->w_temporal; lo.wS = w->w_spatio; lo.bias = w->logit_bias; lo.pool = pool_dev;
+    lo.rw[0] = w->w_router;
+    lo.rw[1] = dv.iT == 1 ? w->w_temporal : (dv.iS == 1 ? w->w_spatio : nullptr);
+    lo.rw[2] = dv.iS == 2 ? w->w_spatio : nullptr;
+    lo.bias = w->logit_bias; lo.pool = pool_dev;
     lo.arena = buf->arena;
     char* sb = static_cast<char*>(buf->state);
     char* wb = static_cast<char*>(buf->workspace);
     lo.cache = reinterpret_cast<unsigned long long*>(sb + p.cache);
     lo.aT = reinterpret_cast<float*>(sb + p.aT);
+    lo.pol = reinterpret_cast<float*>(sb + p.pol);
     lo.pS = reinterpret_cast<float*>(sb + p.pS);
     lo.ctr = reinterpret_cast<int64_t*>(sb + p.ctr);
     lo.phys = reinterpret_cast<int64_t*>(sb + p.phys);
@@ -382,8 +407,9 @@ cmoe_status cmoe_step(cmoe_handle* hd, const void* h, float* y) {
 cmoe_status cmoe_step_logits(cmoe_handle* hd, const float* zR, const float* zT, const float* zS) {
     cmoe_status st = usable(hd);
     if (st != CMOE_OK) return st;
-    if (!zR || !zT) return fail(CMOE_ERR_INVALID_ARG, "zR and zT are required");
-    if (hd->cfg.mode == CMOE_MODE_SPATIO_TEMPORAL && !zS) return fail(CMOE_ERR_INVALID_ARG, "zS is required in full mode");
+    if (!zR) return fail(CMOE_ERR_INVALID_ARG, "zR is required");
+    if (hd->dv.iT > 0 && !zT) return fail(CMOE_ERR_INVALID_ARG, "zT is required with the router policy");
+    if (hd->dv.iS > 0 && !zS) return fail(CMOE_ERR_INVALID_ARG, "zS is required in the modes with a Spatio Router");
     return run_token(hd, nullptr, nullptr, zR, zT, zS);
 }
 
@@ -464,7 +490,7 @@ cmoe_status cmoe_set_R(cmoe_handle* hd, int32_t R) {
     cmoe_status st = usable(hd);
     if (st != CMOE_OK) return st;
     if (R < 0 || R > hd->cfg.N) return fail(CMOE_ERR_INVALID_ARG, "R must be in [0, N]");
-    hd->R = hd->cfg.mode == CMOE_MODE_SPATIO_TEMPORAL ? R : 0;
+    hd->R = has_spatio(hd->cfg.mode) ? R : 0;
     return CMOE_OK;
 }
 
@@ -512,6 +538,7 @@ size_t cmoe_view_bytes(const cmoe_handle* hd, int32_t view) {
         case CMOE_VIEW_EVENTS: return L * S * 4 * 4;
         case CMOE_VIEW_FILLS: return L * 2 * 4;
         case CMOE_VIEW_ACTIVE: return L * 8;
+        case CMOE_VIEW_PRIORITY: return S * L * N * 4;
         default: return 0;
     }
 }
@@ -544,6 +571,7 @@ cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t byte
         case CMOE_VIEW_EVENTS: src = lo.events; break;
         case CMOE_VIEW_FILLS: src = lo.step_fills; break;
         case CMOE_VIEW_ACTIVE: src = lo.active_sum; break;
+        case CMOE_VIEW_PRIORITY: src = lo.pol; break;
     }
     HIPCHK(hipMemcpy(host_out, src, need, hipMemcpyDeviceToHost), "view read");
     return CMOE_OK;

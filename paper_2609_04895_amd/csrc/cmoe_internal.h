@@ -19,18 +19,21 @@ constexpr int kFillBlocks = 128;  // fill kernel workgroups
 // Every pointer the kernels use, carved out of the caller's buffers.
 struct Layout {
     int32_t L, N, K, d, F, C, S, mode, dtype, NW, n_slots, n_r, nsplit, rdk, zstride, warmup;
+    int32_t iT, iS;        // router slot of the Temporal / Spatio Router, -1 if not used
+    int32_t policy;        // retention priority (cmoe_policy)
+    float lrfu_w;          // LRFU decay per token, fl32(2^-lambda)
     int64_t expert_elems;  // 3 d F
-    // weights
-    const void* wR;
-    const void* wT;
-    const void* wS;
+    // weights: router slot r (0 native, then temporal, then spatio, as used)
+    const void* rw[3];
     const float* bias;
     const void* pool;
     // arena: [L][n_slots] experts
     void* arena;
     // state
     unsigned long long* cache;  // [S][L][NW]  cache membership bits
-    float* aT;                  // [S][L][N]   s^T of the previous token (full mode)
+    float* aT;                  // [S][L][N]   previous token's a-score: s^T (full mode),
+                                //             p^R (Spatio-only mode)
+    float* pol;                 // [S][L][N]   classical retention priority
     float* pS;                  // [S][N]      latest Spatio Router distribution
     int64_t* ctr;               // [S][L][kNctr]
     int64_t* phys;              // [L][2]      physical fills: demand, proactive
@@ -38,7 +41,7 @@ struct Layout {
     int32_t* slot_of;           // [2][L][N]   slot of each expert, -1 absent (two versions)
     int32_t* slot_exp;          // [2][L][n_slots] expert in each slot, -1 free
     // workspace
-    double* zpart;              // [S][n_r][N][kMaxSplit] router partial sums
+    double* zpart;              // [S][n_r][N][zstride] router partial sums
     float* logits;              // [L][S][n_r][N]
     int32_t* sel;               // [L][S][K]
     float* gates;               // [L][S][K]
@@ -54,7 +57,7 @@ struct Layout {
 // cache-step kernel flags
 constexpr uint32_t kFlagAccess = 1u;       // route, access, retention for layer l
 constexpr uint32_t kFlagInject = 2u;       // logits come from the caller
-constexpr uint32_t kFlagRefine = 4u;       // refine layer `rl` (full mode)
+constexpr uint32_t kFlagRefine = 4u;       // refine layer `rl` (modes with a Spatio Router)
 constexpr uint32_t kFlagRefinedHere = 8u;  // layer l was refined earlier this token
 constexpr uint32_t kFlagCount = 16u;       // this token is counted
 
@@ -64,9 +67,8 @@ struct StepArgs {
     int32_t R;          // refinement budget
     int32_t bbuf;       // bucket buffer of this layer step (the other one is cleared)
     uint32_t flags;
-    const float* zR;    // injected logits [S][L][N] (kFlagInject)
-    const float* zT;
-    const float* zS;
+    int32_t t;          // token index (LRU clock)
+    const float* z[3];  // injected logits [S][L][N] per router slot (kFlagInject)
 };
 
 // One residency event: layer `layer` must hold the union of the streams'

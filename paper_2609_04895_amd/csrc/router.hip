@@ -66,7 +66,7 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_kernel(Layout lo, in
     const int e_a = et * 16 + r16;  // expert row this lane feeds into A
     const int s_b = st * 16 + r16;  // stream column this lane feeds into B
     const bool va = e_a < lo.N, vb = s_b < lo.S;
-    const void* W = r == 0 ? lo.wR : (r == 1 ? lo.wT : lo.wS);
+    const void* W = lo.rw[r];
     const int64_t arow = ((int64_t)l * lo.N + (va ? e_a : 0)) * lo.d + i0 + 8 * g;
     const int64_t brow = ((int64_t)(vb ? s_b : 0) * lo.L + l) * lo.d + i0 + 8 * g;
 

@@ -10,7 +10,8 @@ from .cmoe import CMOE_FLAG_FILL_ON_MAIN, Engine, make_config
 def config_for(w, C: Optional[int] = None, R: Optional[int] = None, warmup_tokens: int = 0,
                fill_on_main: bool = False):
     return make_config(w.L, w.N, w.K, w.d, w.F, w.C if C is None else C, w.R if R is None else R, w.S, w.mode,
-                       w.dtype, w.pool_kind, warmup_tokens, CMOE_FLAG_FILL_ON_MAIN if fill_on_main else 0)
+                       w.dtype, w.pool_kind, warmup_tokens, CMOE_FLAG_FILL_ON_MAIN if fill_on_main else 0,
+                       w.policy, w.lrfu_lambda)
 
 
 def engine_for(w, inputs, C: Optional[int] = None, R: Optional[int] = None, warmup_tokens: int = 0,
@@ -18,5 +19,5 @@ def engine_for(w, inputs, C: Optional[int] = None, R: Optional[int] = None, warm
     import torch
     cfg = config_for(w, C, R, warmup_tokens, fill_on_main=not side_stream)
     side = torch.cuda.Stream() if side_stream else None
-    return Engine(cfg, inputs["wR"], inputs["wT"], inputs.get("wS"), inputs.get("bias"), inputs["pool"],
+    return Engine(cfg, inputs["wR"], inputs.get("wT"), inputs.get("wS"), inputs.get("bias"), inputs["pool"],
                   side_stream=side)

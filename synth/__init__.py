@@ -24,8 +24,9 @@ from typing import Optional, Tuple
 
 import numpy as np
 
-from .workloads import (DTYPE_BF16, DTYPE_F32, MODE_SPATIO_TEMPORAL, MODE_TEMPORAL,  # noqa: F401
-                        POOL_DEVICE, POOL_HOST_PINNED, WORKLOADS, Workload)
+from .workloads import (DTYPE_BF16, DTYPE_F32, MODE_SPATIO_ONLY, MODE_SPATIO_TEMPORAL,  # noqa: F401
+                        MODE_TEMPORAL, POLICY_LFU, POLICY_LRFU, POLICY_LRU, POLICY_ROUTER, POOL_DEVICE,
+                        POOL_HOST_PINNED, WORKLOADS, Workload)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 CPU_LIB = os.path.join(_HERE, "libsynth_cpu.so")
@@ -233,10 +234,13 @@ def device_inputs(w: Workload, T: Optional[int] = None, with_hidden: bool = True
     dev = torch.device("cuda", torch.cuda.current_device())
     out = {}
     out["wR"] = torch.empty((w.L, w.N, w.d), dtype=dt, device=dev)
-    out["wT"] = torch.empty((w.L, w.N, w.d), dtype=dt, device=dev)
     fill_router_dev(w, KIND_ROUTER_NATIVE, out["wR"].data_ptr(), stream)
-    fill_router_dev(w, KIND_ROUTER_TEMPORAL, out["wT"].data_ptr(), stream)
-    if w.mode == MODE_SPATIO_TEMPORAL:
+    if w.has_temporal:
+        out["wT"] = torch.empty((w.L, w.N, w.d), dtype=dt, device=dev)
+        fill_router_dev(w, KIND_ROUTER_TEMPORAL, out["wT"].data_ptr(), stream)
+    else:
+        out["wT"] = None
+    if w.has_spatio:
         out["wS"] = torch.empty((w.L, w.N, w.d), dtype=dt, device=dev)
         fill_router_dev(w, KIND_ROUTER_SPATIO, out["wS"].data_ptr(), stream)
     else:

@@ -19,6 +19,12 @@ from typing import Optional, Tuple
 
 MODE_TEMPORAL = 0          # update-only Temporal Router (Section 3.2)
 MODE_SPATIO_TEMPORAL = 1   # full mode with pre-access refinement (Section 3.3)
+MODE_SPATIO_ONLY = 2       # Spatio-only ablation (Section 5, Appendix B.4)
+
+POLICY_ROUTER = 0          # retention by the Temporal Router's s^T
+POLICY_LRU = 1             # classical cache-update baselines (Section 4.1, Table 1)
+POLICY_LFU = 2
+POLICY_LRFU = 3
 
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
@@ -48,6 +54,8 @@ class Workload:
     seed: int = 0
     sweep_C: Tuple[int, ...] = ()
     sweep_R: Tuple[int, ...] = ()
+    policy: int = POLICY_ROUTER
+    lrfu_lambda: float = 0.5
 
     @property
     def elem_bytes(self) -> int:
@@ -59,8 +67,16 @@ class Workload:
         return 3 * self.d * self.F * self.elem_bytes
 
     @property
+    def has_temporal(self) -> bool:
+        return self.policy == POLICY_ROUTER
+
+    @property
+    def has_spatio(self) -> bool:
+        return self.mode in (MODE_SPATIO_TEMPORAL, MODE_SPATIO_ONLY)
+
+    @property
     def n_routers(self) -> int:
-        return 3 if self.mode == MODE_SPATIO_TEMPORAL else 2
+        return 1 + int(self.has_temporal) + int(self.has_spatio)
 
     def replace(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)

@@ -17,7 +17,7 @@ def say(*a):
 def clone_run(run: oracle.Run) -> oracle.Run:
     r = copy.copy(run)
     r.cfg = oracle._Cfg(*[getattr(run.cfg, n) for n, _ in oracle._Cfg._fields_])
-    for n in ("cache", "aT", "pS", "ctr", "slot_of", "phys"):
+    for n in ("cache", "aT", "pS", "ctr", "slot_of", "phys", "pol"):
         setattr(r, n, getattr(run, n).copy())
     return r
 
@@ -42,6 +42,41 @@ def compare_step(eng, run: oracle.Run, out: dict, where: str):
     fills = eng.cmoe_read(B.CMOE_VIEW_FILLS)
     assert np.array_equal(fills, out["fills"]), f"{where}: physical fills differ"
     assert np.array_equal(eng.cmoe_read(B.CMOE_VIEW_PHYS), run.phys), f"{where}: physical counters differ"
+    if run.policy != oracle.POLICY_ROUTER:
+        pol = eng.cmoe_read(B.CMOE_VIEW_PRIORITY)
+        assert np.array_equal(pol.view(np.uint32), run.pol.view(np.uint32)), f"{where}: priorities differ"
+
+
+def oracle_logits(w, WR, WT, WS, bias, H, t, streams):
+    """The oracle's fp32 logits of token t, [len(streams)][L][n_r][N], router
+    slots in the library's order (native, temporal if used, spatio if used)."""
+    mats = [WR] + ([WT] if w.has_temporal else []) + ([WS] if w.has_spatio else [])
+    z = np.empty((len(streams), w.L, len(mats), w.N), np.float32)
+    for i, s in enumerate(streams):
+        for l in range(w.L):
+            h = H[(s, l)][t]
+            for r, M in enumerate(mats):
+                z[i, l, r] = oracle.logits(M[l], h, bias[l] if (r == 0 and bias is not None) else None)
+    return z
+
+
+def split_slots(w, z):
+    """(zR, zT or None, zS or None) from [..][L][n_r][N] router-slot logits."""
+    zT = z[:, :, 1] if w.has_temporal else None
+    zS = z[:, :, -1] if w.has_spatio else None
+    return z[:, :, 0], zT, zS
+
+
+def host_routers(w):
+    import synth
+    WR = [synth.router_host(w, synth.KIND_ROUTER_NATIVE, l) for l in range(w.L)]
+    WT = [synth.router_host(w, synth.KIND_ROUTER_TEMPORAL, l) for l in range(w.L)] if w.has_temporal else None
+    WS = [synth.router_host(w, synth.KIND_ROUTER_SPATIO, l) for l in range(w.L)] if w.has_spatio else None
+    return WR, WT, WS
+
+
+def oracle_run(w, **kw):
+    return oracle.Run(w.L, w.N, w.K, w.C, w.R, w.S, w.mode, policy=w.policy, lrfu_lambda=w.lrfu_lambda, **kw)
 
 
 def rel_err(y, ref):

@@ -61,7 +61,14 @@ def test_query_arena_is_capped_by_n_slots():
     (dict(R=17), B.CMOE_ERR_INVALID_ARG),
     (dict(L=0), B.CMOE_ERR_INVALID_ARG),
     (dict(S=0), B.CMOE_ERR_INVALID_ARG),
-    (dict(mode=2), B.CMOE_ERR_INVALID_ARG),
+    (dict(mode=3), B.CMOE_ERR_INVALID_ARG),
+    (dict(mode=2), B.CMOE_ERR_INVALID_ARG),            # Spatio-only has no Temporal Router
+    (dict(policy=4), B.CMOE_ERR_INVALID_ARG),
+    (dict(policy=-1), B.CMOE_ERR_INVALID_ARG),
+    (dict(mode=1, R=2, policy=1), B.CMOE_ERR_UNSUPPORTED),   # full mode retains by s^T
+    (dict(policy=3, lrfu_lambda=-0.5), B.CMOE_ERR_INVALID_ARG),
+    (dict(policy=3, lrfu_lambda=float("nan")), B.CMOE_ERR_INVALID_ARG),
+    (dict(policy=3, lrfu_lambda=float("inf")), B.CMOE_ERR_INVALID_ARG),
     (dict(dtype=5), B.CMOE_ERR_INVALID_ARG),
     (dict(N=300, C=6), B.CMOE_ERR_UNSUPPORTED),
     (dict(d=200), B.CMOE_ERR_UNSUPPORTED),
@@ -72,6 +79,36 @@ def test_query_rejects_invalid_configs(kw, status):
     st, _ = query(**kw)
     assert st == status
     assert len(B.lib().cmoe_last_error()) > 0
+
+
+@pytest.mark.parametrize("kw", [dict(policy=1), dict(policy=2), dict(policy=3, lrfu_lambda=0.0),
+                                dict(mode=2, policy=1, R=3), dict(mode=2, policy=3, R=16)])
+def test_query_accepts_policy_configs(kw):
+    st, out = query(**kw)
+    assert st == B.CMOE_OK
+
+
+def test_classical_policies_need_fewer_router_slots():
+    # one router slot (native) instead of two: smaller partials and logits
+    _, router = query(S=64, N=16, C=6)
+    _, lru = query(S=64, N=16, C=6, policy=1)
+    assert lru.workspace_bytes < router.workspace_bytes
+    assert B.router_slots(cfg(policy=1)) == ["native"]
+    assert B.router_slots(cfg(mode=2, policy=1)) == ["native", "spatio"]
+    assert B.router_slots(cfg(mode=1)) == ["native", "temporal", "spatio"]
+
+
+def test_spatio_only_needs_spatio_router_and_not_temporal():
+    h = ctypes.c_void_p()
+    bufs = B.cmoe_buffers(256, 512, 768)
+    c = cfg(mode=2, policy=1, R=2)
+    w = B.cmoe_weights(256, None, None, None, 1024)
+    st = B.lib().cmoe_init(ctypes.byref(c), ctypes.byref(w), ctypes.byref(bufs), None, None, ctypes.byref(h))
+    assert st == B.CMOE_ERR_INVALID_ARG and b"w_spatio" in B.lib().cmoe_last_error()
+    c = cfg(policy=2)                         # LFU, update-only: W^T is not needed
+    w = B.cmoe_weights(256, None, None, None, 1024)
+    B.lib().cmoe_init(ctypes.byref(c), ctypes.byref(w), ctypes.byref(bufs), None, None, ctypes.byref(h))
+    assert b"w_temporal" not in B.lib().cmoe_last_error()
 
 
 def test_init_rejects_missing_pointers_before_touching_the_gpu():

@@ -16,7 +16,8 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import clone_run, compare_step, rel_err, say
+from gpu_util import (clone_run, compare_step, host_routers, oracle_logits, oracle_run, rel_err, say,
+                      split_slots)
 
 pytestmark = pytest.mark.gpu
 
@@ -62,12 +63,8 @@ def run_e2e(w, T, tol, check_ffn_every=1, samples=None):
     eng = engine_for(w, inp)
     dev = torch.device("cuda", 0)
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device=dev)
-    full = w.mode == synth.MODE_SPATIO_TEMPORAL
-    n_r = 3 if full else 2
     # host copies of what the oracle needs
-    WR = [synth.router_host(w, synth.KIND_ROUTER_NATIVE, l) for l in range(w.L)]
-    WT = [synth.router_host(w, synth.KIND_ROUTER_TEMPORAL, l) for l in range(w.L)]
-    WS = [synth.router_host(w, synth.KIND_ROUTER_SPATIO, l) for l in range(w.L)] if full else None
+    WR, WT, WS = host_routers(w)
     bias = synth.zipf_bias(w)
     H = {(s, l): synth.hidden_host(w, s, l, T=T) for s in range(w.S) for l in range(w.L)}
     experts = {}
@@ -78,7 +75,7 @@ def run_e2e(w, T, tol, check_ffn_every=1, samples=None):
             experts[(l, e)] = synth.expert_host(w, l, e)
         return experts[(l, e)]
 
-    run = oracle.Run(w.L, w.N, w.K, w.C, w.R, w.S, w.mode)
+    run = oracle_run(w)
     ulp_diffs = 0
     near_ties = 0
     worst_ffn = 0.0
@@ -86,14 +83,7 @@ def run_e2e(w, T, tol, check_ffn_every=1, samples=None):
         eng.cmoe_step(inp["hidden"][t], y)
         z_gpu = eng.cmoe_read(B.CMOE_VIEW_LOGITS)      # [L][S][n_r][N]
         # oracle logits from the host twin's inputs
-        z_orc = np.empty((w.S, w.L, n_r, w.N), np.float32)
-        for s in range(w.S):
-            for l in range(w.L):
-                h = H[(s, l)][t]
-                z_orc[s, l, 0] = oracle.logits(WR[l], h, None if bias is None else bias[l])
-                z_orc[s, l, 1] = oracle.logits(WT[l], h)
-                if full:
-                    z_orc[s, l, 2] = oracle.logits(WS[l], h)
+        z_orc = oracle_logits(w, WR, WT, WS, bias, H, t, range(w.S))
         zg = z_gpu.transpose(1, 0, 2, 3)
         diff = zg != z_orc
         if diff.any():
@@ -101,8 +91,8 @@ def run_e2e(w, T, tol, check_ffn_every=1, samples=None):
             assert np.all(gap <= np.spacing(np.abs(z_orc)) * 1.0001), "logit differs by more than one ulp"
             ulp_diffs += int(diff.sum())
         # step-local: decisions from the oracle's own logits vs the GPU's
-        own = clone_run(run).step(z_orc[:, :, 0], z_orc[:, :, 1], z_orc[:, :, 2] if full else None, want="all")
-        out = run.step(zg[:, :, 0], zg[:, :, 1], zg[:, :, 2] if full else None, want="all")
+        own = clone_run(run).step(*split_slots(w, z_orc), want="all")
+        out = run.step(*split_slots(w, zg), want="all")
         compare_step(eng, run, out, f"{w.name} token {t}")
         if not np.array_equal(own["sel"], out["sel"]):
             for s, l in zip(*np.nonzero((own["sel"] != out["sel"]).any(axis=-1))):

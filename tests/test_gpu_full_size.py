@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import rel_err, say
+from gpu_util import host_routers, oracle_logits, oracle_run, rel_err, say, split_slots
 
 pytestmark = pytest.mark.gpu
 
@@ -29,15 +29,11 @@ def run_full(w, T, ffn_samples=8, seed=0):
     inp = synth.device_inputs(w, T=T)
     eng = engine_for(w, inp)
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
-    full = w.mode == synth.MODE_SPATIO_TEMPORAL
-    n_r = 3 if full else 2
     streams = [0, w.S - 1] if w.S > 1 else [0]
-    WR = [synth.router_host(w, synth.KIND_ROUTER_NATIVE, l) for l in range(w.L)]
-    WT = [synth.router_host(w, synth.KIND_ROUTER_TEMPORAL, l) for l in range(w.L)]
-    WS = [synth.router_host(w, synth.KIND_ROUTER_SPATIO, l) for l in range(w.L)] if full else None
+    WR, WT, WS = host_routers(w)
     bias = synth.zipf_bias(w)
     H = {(s, l): synth.hidden_host(w, s, l, T=T) for s in streams for l in range(w.L)}
-    run = oracle.Run(w.L, w.N, w.K, w.C, w.R, len(streams), w.mode)
+    run = oracle_run(w.replace(S=len(streams)))
     rng = np.random.default_rng(seed)
     ffn_at = {(int(rng.integers(T)), int(rng.integers(len(streams))), int(rng.integers(w.L)))
               for _ in range(ffn_samples)}
@@ -48,19 +44,13 @@ def run_full(w, T, ffn_samples=8, seed=0):
         eng.cmoe_step(inp["hidden"][t], y)
         zg_all = eng.cmoe_read(B.CMOE_VIEW_LOGITS)               # [L][S][n_r][N]
         zg = zg_all[:, streams].transpose(1, 0, 2, 3)            # [2][L][n_r][N]
-        for i, s in enumerate(streams):
-            for l in range(w.L):
-                h = H[(s, l)][t]
-                ref = [oracle.logits(WR[l], h, None if bias is None else bias[l]), oracle.logits(WT[l], h)]
-                if full:
-                    ref.append(oracle.logits(WS[l], h))
-                for r in range(n_r):
-                    d = zg[i, l, r] != ref[r]
-                    if d.any():
-                        gap = np.abs(zg[i, l, r].astype(np.float64) - ref[r])
-                        assert np.all(gap <= np.spacing(np.abs(ref[r]))), f"token {t} stream {s} layer {l}"
-                        ulp_diffs += int(d.sum())
-        out = run.step(zg[:, :, 0], zg[:, :, 1], zg[:, :, 2] if full else None, want="all")
+        ref = oracle_logits(w, WR, WT, WS, bias, H, t, streams)   # [2][L][n_r][N]
+        d = zg != ref
+        if d.any():
+            gap = np.abs(zg.astype(np.float64) - ref)
+            assert np.all(gap <= np.spacing(np.abs(ref))), f"token {t}: logit differs by more than one ulp"
+            ulp_diffs += int(d.sum())
+        out = run.step(*split_slots(w, zg), want="all")
         sel = eng.cmoe_read(B.CMOE_VIEW_SELECTED)                 # [L][S][K]
         assert np.array_equal(sel[:, streams].transpose(1, 0, 2), out["sel"]), f"token {t}: selections"
         cache = eng.cache_sets()                                   # [S][L][N]
@@ -72,7 +62,7 @@ def run_full(w, T, ffn_samples=8, seed=0):
         # invariants over all streams
         assert np.all(ev[:, :, 0] + ev[:, :, 1] == w.K), f"token {t}: hits + misses != K"
         assert np.all(cache.sum(axis=-1) <= w.C), f"token {t}: cache over capacity"
-        assert np.all(ev[:, :, 2] <= (w.R if full else 0)), f"token {t}: too many proactive loads"
+        assert np.all(ev[:, :, 2] <= (w.R if w.has_spatio else 0)), f"token {t}: too many proactive loads"
         for (tt, i, l) in ffn_at:
             if tt != t:
                 continue
@@ -96,7 +86,7 @@ def run_full(w, T, ffn_samples=8, seed=0):
     assert tot["tokens"] == w.S * T
     assert tot["traffic_bytes"] == (tot["demand_misses"] + tot["proactive_loads"]) * w.expert_bytes
     assert tot["phys_fills"] <= tot["demand_misses"] + tot["proactive_loads"]
-    if not full or w.R == 0:
+    if not w.has_spatio or w.R == 0:
         assert tot["proactive_loads"] == 0
     say(f"{w.name}: ok; one-ulp logit differences {ulp_diffs}; worst FFN error {worst:.3g}; "
         f"hit {1 - tot['demand_misses'] / tot['accesses']:.4f}; proactive {tot['proactive_loads']}; "
