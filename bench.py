@@ -114,6 +114,8 @@ def main():
                     help="retention priority (default: the workload's, the Temporal Router)")
     ap.add_argument("--mode", choices=sorted(MODES), default=None, help="default: the workload's mode")
     ap.add_argument("--lrfu-lambda", type=float, default=None)
+    ap.add_argument("--layers", type=int, default=None,
+                    help="run the first L layers only (a pinned-host pool larger than the host allows)")
     ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
     ap.add_argument("--no-profile", action="store_true", help="no per-kernel HIP events in the timed region")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
@@ -142,6 +144,8 @@ def main():
         w = w.replace(mode=MODES[args.mode])
     if args.lrfu_lambda is not None:
         w = w.replace(lrfu_lambda=args.lrfu_lambda)
+    if args.layers is not None:
+        w = w.replace(L=args.layers)
     warmup = args.warmup
     steps = args.steps if args.steps is not None else max(1, w.T - warmup)
     T_gen = min(w.T, warmup + steps)
