@@ -37,7 +37,8 @@ class _Cfg(ctypes.Structure):
 
 class _State(ctypes.Structure):
     _fields_ = [("cache", _u8p), ("aT", _f32p), ("pS", _f32p), ("ctr", _i64p), ("slot_of", _i32p),
-                ("phys", _i64p), ("pol", _f32p), ("n_slots", ctypes.c_int32), ("t", ctypes.c_int32)]
+                ("phys", _i64p), ("pol", _f32p), ("selcount", _i64p), ("n_slots", ctypes.c_int32),
+                ("t", ctypes.c_int32)]
 
 
 class _Out(ctypes.Structure):
@@ -67,6 +68,8 @@ def lib():
         L.orc_moe_ffn.argtypes = [_f32p, _f32p, _f32p, _f64p, ctypes.c_int, _f32p, ctypes.c_int,
                                   ctypes.c_int, _f64p]
         L.orc_metrics.argtypes = [ctypes.c_int64] * 4 + [ctypes.c_double, _f64p]
+        L.orc_concentration.argtypes = [_i64p, ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64p]
+        L.orc_concentration.restype = ctypes.c_int
         L.orc_lrfu_weight.argtypes = [ctypes.c_float]
         L.orc_lrfu_weight.restype = ctypes.c_float
         L.orc_step.argtypes = [ctypes.POINTER(_Cfg), ctypes.POINTER(_State), _f32p, _f32p, _f32p,
@@ -160,6 +163,18 @@ def moe_ffn(Wg, Wu, Wd, gates, x) -> np.ndarray:
     return y
 
 
+def concentration(counts, top_m: int = 8):
+    """Per-layer expert-use concentration of selection counts [L][N], averaged
+    over layers: (effective experts exp(H), entropy H in nats, max frequency,
+    top-m mass)."""
+    c = np.ascontiguousarray(counts, dtype=np.int64)
+    if c.ndim == 1:
+        c = c[None]
+    out = np.zeros(4, dtype=np.float64)
+    lib().orc_concentration(_p(c, _i64p), c.shape[0], c.shape[1], int(top_m), _p(out, _f64p))
+    return tuple(float(v) for v in out)
+
+
 def metrics(A: int, D: int, P: int, T: int, expert_bytes: float):
     """(Hit, AdjHit, Load in MB per decode token)."""
     out = np.zeros(3, dtype=np.float64)
@@ -185,6 +200,7 @@ class Run:
         self.L, self.N, self.K, self.C, self.S, self.mode = L, N, K, C, S, mode
         self.policy = policy
         self.pol = np.zeros((S, L, N), dtype=np.float32)
+        self.selcount = np.zeros((L, N), dtype=np.int64)
         self.cache = np.zeros((S, L, N), dtype=np.uint8)
         self.aT = np.zeros((S, L, N), dtype=np.float32)
         self.pS = np.zeros((S, N), dtype=np.float32)
@@ -203,7 +219,8 @@ class Run:
 
     def _state(self):
         return _State(_p(self.cache, _u8p), _p(self.aT, _f32p), _p(self.pS, _f32p), _p(self.ctr, _i64p),
-                      _p(self.slot_of, _i32p), _p(self.phys, _i64p), _p(self.pol, _f32p), self.n_slots, self.t)
+                      _p(self.slot_of, _i32p), _p(self.phys, _i64p), _p(self.pol, _f32p), _p(self.selcount, _i64p),
+                      self.n_slots, self.t)
 
     def step(self, zR, zT=None, zS=None, want=("sel", "gate")):
         """zR, zT, zS: [S][L][N] float32 (zT only for the router policy in the

@@ -21,6 +21,10 @@
  *     recency; frequency counts; Lee et al. 2001 for the combined
  *     recency-frequency value with weighing function (1/2)^(lambda x)), as
  *     the retention priority of the same post-access update (Algorithm 1)
+ *   - expert-use concentration of the native selections (Section 5,
+ *     "routing behaviour" figure): per layer the selection frequencies f_e
+ *     (normalised to sum 1), effective experts exp(H), entropy H in nats,
+ *     max frequency and top-m mass, averaged over layers
  *   - the Spatio-only ablation (Section 5 ablations, Appendix B.4):
  *     s^S = p^R_{t-1,l} + p^S_rho drives the pre-access refinement, and
  *     demand-miss insertion evicts by LRU
@@ -272,6 +276,46 @@ void orc_moe_ffn(const float* Wg, const float* Wu, const float* Wd, const double
     free(act);
 }
 
+/* Expert-use concentration from per-(layer, expert) selection counts
+ * [L][N]: for each layer with at least one selection, f_e = count_e / sum,
+ * H = -sum_{f_e > 0} f_e ln f_e, and out4 = the means over those layers of
+ * exp(H), H, max_e f_e and the sum of the top_m largest f_e.  Returns the
+ * number of layers averaged. */
+int orc_concentration(const int64_t* counts, int L, int N, int top_m, double* out4) {
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    int used = 0;
+    for (int l = 0; l < L; ++l) {
+        const int64_t* c = counts + (size_t)l * N;
+        int64_t tot = 0;
+        for (int e = 0; e < N; ++e) tot += c[e];
+        if (tot == 0) continue;
+        double f[ORC_NMAX], H = 0.0, fmax = 0.0;
+        for (int e = 0; e < N; ++e) {
+            f[e] = (double)c[e] / (double)tot;
+            if (f[e] > 0.0) H -= f[e] * log(f[e]);
+            if (f[e] > fmax) fmax = f[e];
+        }
+        /* top-m mass: repeatedly take the largest remaining frequency */
+        uint8_t taken[ORC_NMAX];
+        memset(taken, 0, (size_t)N);
+        double mass = 0.0;
+        for (int i = 0; i < top_m && i < N; ++i) {
+            int best = -1;
+            for (int e = 0; e < N; ++e)
+                if (!taken[e] && (best < 0 || f[e] > f[best])) best = e;
+            taken[best] = 1;
+            mass += f[best];
+        }
+        acc[0] += exp(H);
+        acc[1] += H;
+        acc[2] += fmax;
+        acc[3] += mass;
+        ++used;
+    }
+    for (int i = 0; i < 4; ++i) out4[i] = used ? acc[i] / used : 0.0;
+    return used;
+}
+
 /* Hit = 1 - D/A, AdjHit = (A - D)/(A + P), Load/token = (D + P) S_exp / T in
  * decimal MB (Section 4.1 "Metrics"). */
 void orc_metrics(int64_t A, int64_t D, int64_t P, int64_t T, double expert_bytes, double* out3) {
@@ -303,6 +347,7 @@ typedef struct {
     int32_t* slot_of; /* [L][N]    physical slot of each expert, -1 = absent   */
     int64_t* phys;    /* [L][2]    physical fills: demand, proactive (counted)  */
     float* pol;       /* [S][L][N] classical retention priority (policy != 0)  */
+    int64_t* selcount;/* [L][N]    native selections per expert (counted tokens) */
     int32_t n_slots;  /* physical slots per layer                              */
     int32_t t;        /* index of the next token                               */
 } orc_state;
@@ -443,6 +488,7 @@ int orc_step(const orc_cfg* c, orc_state* st, const float* zR, const float* zT, 
                 memcpy(st->pS + (size_t)s * N, pSn, sizeof(float) * (size_t)N);
             }
             if (counted) {
+                for (int k = 0; k < K; ++k) st->selcount[(size_t)l * N + sel[k]] += 1;
                 int64_t* ctr = st->ctr + sl * ORC_NCTR;
                 ctr[ORC_CTR_A] += K;
                 ctr[ORC_CTR_HITS] += hits;
