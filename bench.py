@@ -226,6 +226,8 @@ def main():
     res["cache"] = {"hit": 1 - D / A, "adj_hit": (A - D) / (A + P), "load_mb_per_token": (D + P) * w.expert_bytes
                     / 1e6 / Tc, "accesses": A, "demand_misses": D, "proactive_loads": P, "tokens": Tc,
                     "phys_fills": tot["phys_fills"], "distinct_experts_per_layer_step": n_act / launches}
+    eff, ent, fmax, top8 = eng.cmoe_concentration(8)
+    res["concentration"] = {"effective_experts": eff, "entropy_nats": ent, "max_frequency": fmax, "top8_mass": top8}
     print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
     eng.cmoe_destroy()
     del inputs, hidden

@@ -218,7 +218,9 @@ cmoe_status cmoe_destroy(cmoe_handle* hd);
  *   CMOE_VIEW_ACTIVE    int64 [L] distinct experts executed by the FFN, summed
  *                              over counted tokens (each is one read of its weights)
  *   CMOE_VIEW_PRIORITY  fp32  [S][L][N] classical retention priority (LRU time,
- *                              LFU count, LRFU value); zeros with the router policy */
+ *                              LFU count, LRFU value); zeros with the router policy
+ *   CMOE_VIEW_SELCOUNT  u64   [L][N] native selections of each expert, summed over
+ *                              streams and counted tokens */
 enum {
     CMOE_VIEW_LOGITS = 0,
     CMOE_VIEW_SELECTED = 1,
@@ -231,7 +233,8 @@ enum {
     CMOE_VIEW_FILLS = 8,
     CMOE_VIEW_ACTIVE = 9,
     CMOE_VIEW_PRIORITY = 10,
-    CMOE_VIEW_COUNT = 11
+    CMOE_VIEW_SELCOUNT = 11,
+    CMOE_VIEW_COUNT = 12
 };
 
 /* Bytes of a view (0 for an unknown view or a NULL handle). */
@@ -253,6 +256,14 @@ cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t byte
 #define CMOE_KERNEL_COUNT 6
 cmoe_status cmoe_profile_begin(cmoe_handle* hd, int32_t max_tokens, uint32_t kernel_mask);
 cmoe_status cmoe_profile_end(cmoe_handle* hd, double* ms_out, int64_t* launches_out);
+
+/* Expert-use concentration of the native selections so far (Section 5,
+ * routing behaviour): per layer with at least one counted selection, the
+ * selection frequencies f_e (summing to 1), entropy H = -sum f_e ln f_e;
+ * out4 = the means over those layers of {exp(H) (effective experts), H,
+ * max_e f_e, the sum of the top_m largest f_e} (the paper uses top_m = 8).
+ * All zeros before any counted token.  Synchronizes. */
+cmoe_status cmoe_concentration(cmoe_handle* hd, int32_t top_m, double* out4);
 
 const char* cmoe_last_error(void);
 

@@ -46,12 +46,13 @@ CMOE_VIEW_EVENTS = 7
 CMOE_VIEW_FILLS = 8
 CMOE_VIEW_ACTIVE = 9
 CMOE_VIEW_PRIORITY = 10
+CMOE_VIEW_SELCOUNT = 11
 CMOE_KERNEL_COUNT = 6
 KERNEL_NAMES = ("router", "cache_step", "fill", "ffn_up", "ffn_down", "combine")
 
 EXPORTED = ("cmoe_query", "cmoe_init", "cmoe_step", "cmoe_step_logits", "cmoe_stats", "cmoe_get_cache",
             "cmoe_set_cache", "cmoe_set_R", "cmoe_reset", "cmoe_destroy", "cmoe_view_bytes", "cmoe_read",
-            "cmoe_profile_begin", "cmoe_profile_end", "cmoe_last_error")
+            "cmoe_profile_begin", "cmoe_profile_end", "cmoe_concentration", "cmoe_last_error")
 
 
 class cmoe_config(ctypes.Structure):
@@ -115,6 +116,7 @@ def lib():
         L.cmoe_read.argtypes = [vp, i32, vp, ctypes.c_size_t]
         L.cmoe_profile_begin.argtypes = [vp, i32, ctypes.c_uint32]
         L.cmoe_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_double), i64p]
+        L.cmoe_concentration.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double)]
         L.cmoe_last_error.argtypes = []
         L.cmoe_last_error.restype = ctypes.c_char_p
         for n in EXPORTED:
@@ -237,9 +239,17 @@ class Engine:
             CMOE_VIEW_FILLS: (np.int32, (c.L, 2)),
             CMOE_VIEW_ACTIVE: (np.int64, (c.L,)),
             CMOE_VIEW_PRIORITY: (np.float32, (c.S, c.L, c.N)),
+            CMOE_VIEW_SELCOUNT: (np.uint64, (c.L, c.N)),
         }
         dt, shape = shapes[view]
         return raw.view(dt).reshape(shape)
+
+    def cmoe_concentration(self, top_m: int = 8):
+        """(effective experts, entropy in nats, max frequency, top-m mass),
+        layer means of the native selection frequencies."""
+        out = (ctypes.c_double * 4)()
+        _check(lib().cmoe_concentration(self.handle, int(top_m), out))
+        return tuple(float(v) for v in out)
 
     def cache_sets(self) -> np.ndarray:
         """Cache membership as a bool array [S][L][N]."""

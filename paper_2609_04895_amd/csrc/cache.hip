@@ -470,7 +470,10 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             const int64_t be = (int64_t)a.bbuf * N + my_sel;
             const int pos = atomicAdd(&lo.bcount[be], 1);
             lo.pairs[be * lo.S + pos] = (s << 8) | lane;
-            if (pos == 0 && counted) atomicAdd(&lo.active_sum[l], 1ull);
+            if (counted) {
+                if (pos == 0) atomicAdd(&lo.active_sum[l], 1ull);
+                atomicAdd(&lo.selcount[(int64_t)l * N + my_sel], 1ull);
+            }
         }
         // retention priority of Algorithm 1
         float sT[NPL];
@@ -595,6 +598,7 @@ __global__ void init_kernel(Layout lo) {
         lo.step_fills[i] = 0;
     }
     for (int64_t i = gid; i < lo.L; i += gs) lo.active_sum[i] = 0ull;
+    for (int64_t i = gid; i < (int64_t)lo.L * lo.N; i += gs) lo.selcount[i] = 0ull;
     for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.N; i += gs) lo.slot_of[i] = -1;
     for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.n_slots; i += gs) lo.slot_exp[i] = -1;
     for (int64_t i = gid; i < (int64_t)lo.L * lo.S * 4; i += gs) lo.events[i] = 0;

@@ -101,7 +101,7 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
 
 // Offsets of every sub-buffer; used both for sizing and for carving.
 struct Plan {
-    size_t cache, aT, pol, pS, ctr, phys, active_sum, slot_of, slot_exp, state_total;
+    size_t cache, aT, pol, pS, ctr, phys, active_sum, selcount, slot_of, slot_exp, state_total;
     size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, zero_row, ws_total;
     size_t arena;
 };
@@ -122,6 +122,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.ctr = take(S * L * cmoe::kNctr * 8);
     p.phys = take(L * 2 * 8);
     p.active_sum = take(L * 8);
+    p.selcount = take(L * N * 8);
     p.slot_of = take(2 * L * N * 4);
     p.slot_exp = take(2 * L * (size_t)dv.n_slots * 4);
     p.state_total = o;
@@ -365,6 +366,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.ctr = reinterpret_cast<int64_t*>(sb + p.ctr);
     lo.phys = reinterpret_cast<int64_t*>(sb + p.phys);
     lo.active_sum = reinterpret_cast<unsigned long long*>(sb + p.active_sum);
+    lo.selcount = reinterpret_cast<unsigned long long*>(sb + p.selcount);
     lo.slot_of = reinterpret_cast<int32_t*>(sb + p.slot_of);
     lo.slot_exp = reinterpret_cast<int32_t*>(sb + p.slot_exp);
     lo.zpart = reinterpret_cast<double*>(wb + p.zpart);
@@ -539,6 +541,7 @@ size_t cmoe_view_bytes(const cmoe_handle* hd, int32_t view) {
         case CMOE_VIEW_FILLS: return L * 2 * 4;
         case CMOE_VIEW_ACTIVE: return L * 8;
         case CMOE_VIEW_PRIORITY: return S * L * N * 4;
+        case CMOE_VIEW_SELCOUNT: return L * N * 8;
         default: return 0;
     }
 }
@@ -572,6 +575,7 @@ cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t byte
         case CMOE_VIEW_FILLS: src = lo.step_fills; break;
         case CMOE_VIEW_ACTIVE: src = lo.active_sum; break;
         case CMOE_VIEW_PRIORITY: src = lo.pol; break;
+        case CMOE_VIEW_SELCOUNT: src = lo.selcount; break;
     }
     HIPCHK(hipMemcpy(host_out, src, need, hipMemcpyDeviceToHost), "view read");
     return CMOE_OK;
@@ -615,6 +619,42 @@ cmoe_status cmoe_profile_end(cmoe_handle* hd, double* ms_out, int64_t* launches_
     hd->prof_rec.clear();
     hd->prof_next = 0;
     hd->prof_left = 0;
+    return CMOE_OK;
+}
+
+cmoe_status cmoe_concentration(cmoe_handle* hd, int32_t top_m, double* out4) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    if (!out4 || top_m < 1) return fail(CMOE_ERR_INVALID_ARG, "need top_m >= 1 and an output array");
+    st = sync_all(hd);
+    if (st != CMOE_OK) return st;
+    const int L = hd->cfg.L, N = hd->cfg.N;
+    std::vector<uint64_t> cnt((size_t)L * N);
+    HIPCHK(hipMemcpy(cnt.data(), hd->lo.selcount, cnt.size() * 8, hipMemcpyDeviceToHost), "selection counts read");
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    int used = 0;
+    std::vector<double> f(N);
+    for (int l = 0; l < L; ++l) {
+        const uint64_t* c = &cnt[(size_t)l * N];
+        uint64_t tot = 0;
+        for (int e = 0; e < N; ++e) tot += c[e];
+        if (tot == 0) continue;
+        double H = 0.0;
+        for (int e = 0; e < N; ++e) {
+            f[e] = (double)c[e] / (double)tot;
+            if (f[e] > 0.0) H -= f[e] * std::log(f[e]);
+        }
+        std::vector<double> sorted(f);
+        std::sort(sorted.begin(), sorted.end(), [](double a, double b) { return a > b; });
+        double mass = 0.0;
+        for (int i = 0; i < top_m && i < N; ++i) mass += sorted[i];
+        acc[0] += std::exp(H);
+        acc[1] += H;
+        acc[2] += sorted[0];
+        acc[3] += mass;
+        ++used;
+    }
+    for (int i = 0; i < 4; ++i) out4[i] = used ? acc[i] / used : 0.0;
     return CMOE_OK;
 }
 

@@ -38,6 +38,7 @@ struct Layout {
     int64_t* ctr;               // [S][L][kNctr]
     int64_t* phys;              // [L][2]      physical fills: demand, proactive
     unsigned long long* active_sum;  // [L]    distinct experts executed (counted tokens)
+    unsigned long long* selcount;    // [L][N] native selections per expert (counted tokens)
     int32_t* slot_of;           // [2][L][N]   slot of each expert, -1 absent (two versions)
     int32_t* slot_exp;          // [2][L][n_slots] expert in each slot, -1 free
     // workspace

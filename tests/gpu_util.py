@@ -17,7 +17,7 @@ def say(*a):
 def clone_run(run: oracle.Run) -> oracle.Run:
     r = copy.copy(run)
     r.cfg = oracle._Cfg(*[getattr(run.cfg, n) for n, _ in oracle._Cfg._fields_])
-    for n in ("cache", "aT", "pS", "ctr", "slot_of", "phys", "pol"):
+    for n in ("cache", "aT", "pS", "ctr", "slot_of", "phys", "pol", "selcount"):
         setattr(r, n, getattr(run, n).copy())
     return r
 
@@ -42,6 +42,10 @@ def compare_step(eng, run: oracle.Run, out: dict, where: str):
     fills = eng.cmoe_read(B.CMOE_VIEW_FILLS)
     assert np.array_equal(fills, out["fills"]), f"{where}: physical fills differ"
     assert np.array_equal(eng.cmoe_read(B.CMOE_VIEW_PHYS), run.phys), f"{where}: physical counters differ"
+    selcount = eng.cmoe_read(B.CMOE_VIEW_SELCOUNT)
+    assert np.array_equal(selcount.astype(np.int64), run.selcount), f"{where}: selection counts differ"
+    conc = eng.cmoe_concentration(8)
+    assert np.allclose(conc, oracle.concentration(run.selcount, 8), rtol=1e-12, atol=1e-15), f"{where}: concentration"
     if run.policy != oracle.POLICY_ROUTER:
         pol = eng.cmoe_read(B.CMOE_VIEW_PRIORITY)
         assert np.array_equal(pol.view(np.uint32), run.pol.view(np.uint32)), f"{where}: priorities differ"
