@@ -102,6 +102,84 @@ def cpu_baseline(w, budget_s):
                       f"SwiGLU FFN of the {w.K} selected experts), single thread, {busy:.1f} s of oracle time"}
 
 
+def run_config(w, inputs, warmup, steps, profile_fill=False):
+    """One configuration through the C ABI: untimed warm-up tokens, then
+    `steps` timed tokens.  Returns (seconds per token, stats, fill ms, fill
+    launches)."""
+    import torch
+
+    from paper_2609_04895_amd.workload import engine_for
+    eng = engine_for(w, inputs, warmup_tokens=warmup)
+    hidden = inputs["hidden"]
+    y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
+    for t in range(warmup):
+        eng.cmoe_step(hidden[t], y)
+    torch.cuda.synchronize()
+    if profile_fill:
+        eng.cmoe_profile_begin(steps, kernels=("fill",))
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(eng.main_stream)
+    for t in range(warmup, warmup + steps):
+        eng.cmoe_step(hidden[t], y)
+    ev1.record(eng.main_stream)
+    torch.cuda.synchronize()
+    sec = ev0.elapsed_time(ev1) / 1e3 / steps
+    prof = eng.cmoe_profile_end() if profile_fill else None
+    tot, _, _ = eng.cmoe_stats()
+    eng.cmoe_destroy()
+    fill_ms, fill_n = prof["fill"] if prof else (0.0, 0)
+    return sec, tot, fill_ms, fill_n
+
+
+def overlap_study(w, warmup, steps):
+    """Exposed expert-loading time per decode token against Appendix B.3's
+    fixed-trace model t_load(eta) = c_exp / T [D + (1 - eta) P], on one stream
+    whose every logical load is a physical copy from the cold pool.
+
+    Configurations on the same inputs: A = the workload (full mode, demand and
+    proactive loads; proactive copies on the side stream overlap the previous
+    layer's FFN), B = update-only (demand loads only, all on the critical
+    path), Z = capacity N (after warm-up nearly every expert stays resident:
+    the compute time of the same decode).  c_exp, the time of one expert copy,
+    and the launch cost of a fill with nothing to copy, solve fill time =
+    launches x t0 + copies x c_exp over the fill kernel's HIP events in B and Z.  The exposed load of a configuration is its time per
+    token minus Z's, corrected for Z's few remaining copies."""
+    import synth
+    T = warmup + steps
+    inputs = synth.device_inputs(w, T=T)
+    cfgA = w
+    cfgB = w.replace(mode=synth.MODE_TEMPORAL, R=0)
+    cfgZ = w.replace(mode=synth.MODE_TEMPORAL, R=0, C=w.N)
+    res = {}
+    for name, cw, prof in (("A", cfgA, False), ("B", cfgB, False), ("B_fill_events", cfgB, True),
+                           ("Z", cfgZ, False), ("Z_fill_events", cfgZ, True)):
+        sec, tot, fill_ms, fill_n = run_config(cw, inputs, warmup, steps, profile_fill=prof)
+        A_, D_, P_, Tc = tot["accesses"], tot["demand_misses"], tot["proactive_loads"], tot["tokens"]
+        res[name] = {"ms_per_token": sec * 1e3, "A": A_, "D": D_, "P": P_, "T": Tc,
+                     "phys_fills": tot["phys_fills"], "hit": 1 - D_ / A_, "adj_hit": (A_ - D_) / (A_ + P_),
+                     "load_mb_per_token": (D_ + P_) * w.expert_bytes / 1e6 / Tc,
+                     "fill_ms": fill_ms, "fill_launches": fill_n}
+        print(f"[overlap] {name}: {res[name]}", file=sys.stderr, flush=True)
+    B, Bf, Z, Zf = res["B"], res["B_fill_events"], res["Z"], res["Z_fill_events"]
+    # fill time = launches x t0 + copies x c_exp, from the two event runs
+    nB, FB, nZ, FZ = Bf["fill_launches"], Bf["phys_fills"], Zf["fill_launches"], Zf["phys_fills"]
+    c_exp = (Bf["fill_ms"] - Zf["fill_ms"] * nB / nZ) / (FB - FZ * nB / nZ)
+    t0 = (Zf["fill_ms"] - FZ * c_exp) / nZ
+    # Z still copies a few first-time experts; charge them at c_exp
+    compute = Z["ms_per_token"] - Z["phys_fills"] * c_exp / Z["T"]
+    out = {"study": "transfer overlap (Appendix B.3)", "workload": describe(w), "warmup": warmup, "steps": steps,
+           "expert_bytes": w.expert_bytes, "c_exp_ms": c_exp, "copy_GBs": w.expert_bytes / (c_exp / 1e3) / 1e9,
+           "empty_fill_launch_ms": t0, "compute_ms_per_token": compute, "configs": res}
+    for name in ("A", "B"):
+        r = res[name]
+        exposed = r["ms_per_token"] - compute
+        lo_, hi_ = r["D"] * c_exp / r["T"], (r["D"] + r["P"]) * c_exp / r["T"]
+        eta = 1.0 - (exposed - lo_) / (hi_ - lo_) if r["P"] > 0 else None
+        out[name] = {"exposed_ms_per_token": exposed, "t_load_eta1_ms": lo_, "t_load_eta0_ms": hi_,
+                     "eta_implied": eta}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -119,6 +197,9 @@ def main():
     ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
     ap.add_argument("--no-profile", action="store_true", help="no per-kernel HIP events in the timed region")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
+    ap.add_argument("--overlap-study", action="store_true",
+                    help="instead of the benchmark line: measure exposed expert-loading time per token and the "
+                         "transfer-overlap model of Appendix B.3 (use with --workload qwen3_30b_s1)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the timed region, run one elementwise device copy of 1 GiB (reference "
                          "kernel for scaling rocprofv3 byte counters)")
@@ -148,6 +229,9 @@ def main():
         w = w.replace(L=args.layers)
     warmup = args.warmup
     steps = args.steps if args.steps is not None else max(1, w.T - warmup)
+    if args.overlap_study:
+        print(json.dumps(overlap_study(w, warmup, min(steps, w.T - warmup))), flush=True)
+        return
     T_gen = min(w.T, warmup + steps)
     print(f"[bench] {describe(w)}; warmup {warmup}, timed {steps}", file=sys.stderr, flush=True)
 

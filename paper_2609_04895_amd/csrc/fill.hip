@@ -52,42 +52,45 @@ __device__ int block_scan(int v, int* total, int* lds4) {
 //   down part, units [F d / 4, 3 F d / 8):
 //     F d / 4 + ((((dt * (F/64) + c) * 2 + mt) * 2 + half) * 64 + lane)
 //     = W_down[32 dt + 16 mt + lane % 16][64 c + 16 (lane / 16) + 8 half .. + 8]
-// The cold pool keeps the plain row-major layout; this maps a slot unit to
-// its pool unit.
-__device__ inline int64_t packed_source_unit(int u, int d, int F) {
-    const int partA = F / 16 * (d / 64) * 256;
-    int lane, half, sub, c, tile, row, col, rows_per_tile, ncol_chunks;
-    int64_t base;
-    if (u < partA) {
-        ncol_chunks = d / 64;
-        rows_per_tile = 16;
-        lane = u & 63;
-        int t = u >> 6;
-        half = t & 1;
-        t >>= 1;
-        sub = t & 1;  // gate or up
-        t >>= 1;
-        c = t % ncol_chunks;
-        tile = t / ncol_chunks;
-        row = rows_per_tile * tile + (lane & 15);
-        col = 64 * c + 16 * (lane >> 4) + 8 * half;
-        base = (int64_t)sub * F * d + (int64_t)row * d + col;
+// The cold pool keeps the plain row-major layout.  Every 128-unit block of
+// the packed order (one run for each half) holds 16 source rows x 128
+// contiguous bytes: rows 16 ft + r of W_mat at columns 64 c .. 64 c + 63 for
+// the gate/up part, rows 32 dt + 16 mt + r of W_down at columns 64 c .. for
+// the down part.  The copy walks the source side of a block in order (8
+// consecutive lanes read one 128-byte row segment, so the reads are long and
+// contiguous, which matters for a pool in pinned host memory read over the
+// host link) and writes each 16-byte unit to its packed position inside the
+// block's contiguous 2 KB.
+struct BlockMap {
+    int64_t src;  // source unit of row 0, chunk 0 of the block
+    int64_t row;  // source units between consecutive rows
+};
+
+__device__ inline BlockMap packed_block(int b, int d, int F) {
+    const int partA = F / 16 * (d / 64) * 2;  // gate/up blocks
+    BlockMap m;
+    if (b < partA) {
+        const int sub = b & 1;  // gate or up
+        const int t = b >> 1;
+        const int c = t % (d / 64), tile = t / (d / 64);
+        m.src = ((int64_t)sub * F * d + (int64_t)16 * tile * d + 64 * c) / 8;
+        m.row = d / 8;
     } else {
-        const int v = u - partA;
-        ncol_chunks = F / 64;
-        lane = v & 63;
-        int t = v >> 6;
-        half = t & 1;
-        t >>= 1;
-        sub = t & 1;  // 16-row half of the 32-row tile
-        t >>= 1;
-        c = t % ncol_chunks;
-        tile = t / ncol_chunks;
-        row = 32 * tile + 16 * sub + (lane & 15);
-        col = 64 * c + 16 * (lane >> 4) + 8 * half;
-        base = 2 * (int64_t)F * d + (int64_t)row * F + col;
+        const int v = b - partA;
+        const int sub = v & 1;  // 16-row half of the 32-row tile
+        const int t = v >> 1;
+        const int c = t % (F / 64), tile = t / (F / 64);
+        m.src = (2 * (int64_t)F * d + (int64_t)(32 * tile + 16 * sub) * F + 64 * c) / 8;
+        m.row = F / 8;
     }
-    return base / 8;
+    return m;
+}
+
+// Source unit w of a block (row w / 8, 16-byte chunk w % 8 of the row's 128
+// bytes) goes to packed unit (chunk % 2) * 64 + row + 16 (chunk / 2).
+__device__ inline int packed_dest_in_block(int w) {
+    const int r = w >> 3, j = w & 7;
+    return (j & 1) * 64 + r + 16 * (j >> 1);
 }
 
 __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
@@ -152,7 +155,11 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
             reinterpret_cast<const uint4*>(static_cast<const char*>(lo.pool) + ((int64_t)layer * N + ex) * bytes);
         uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(lo.arena) + ((int64_t)layer * lo.n_slots + q) * bytes);
         if (lo.dtype == 1) {
-            for (int64_t i = gid; i < n16; i += gs) dst[i] = src[packed_source_unit((int)i, lo.d, lo.F)];
+            for (int64_t i = gid; i < n16; i += gs) {
+                const int b = (int)(i >> 7), w = (int)(i & 127);
+                const BlockMap m = packed_block(b, lo.d, lo.F);
+                dst[(int64_t)b * 128 + packed_dest_in_block(w)] = src[m.src + (w >> 3) * m.row + (w & 7)];
+            }
         } else {
             for (int64_t i = gid; i < n16; i += gs) dst[i] = src[i];
         }

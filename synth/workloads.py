@@ -103,4 +103,9 @@ WORKLOADS = {
     "qwen3_235b_slice": Workload("qwen3_235b_slice", L=16, N=128, K=8, d=4096, F=1536, C=32, R=4,
                                  S=256, T=256, mode=MODE_SPATIO_TEMPORAL, dtype=DTYPE_BF16, rho=0.9,
                                  pool_kind=POOL_HOST_PINNED),
+    # One decode stream at the Qwen3-30B-A3B shape with the cold pool in
+    # pinned host memory: every logical load is a physical copy over the host
+    # link (the transfer-overlap study of Appendix B.3).
+    "qwen3_30b_s1": Workload("qwen3_30b_s1", L=48, N=128, K=8, d=2048, F=768, C=32, R=4, S=1, T=256,
+                             mode=MODE_SPATIO_TEMPORAL, dtype=DTYPE_BF16, rho=0.9, pool_kind=POOL_HOST_PINNED),
 }
