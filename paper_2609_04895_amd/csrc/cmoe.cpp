@@ -102,9 +102,13 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
 // Offsets of every sub-buffer; used both for sizing and for carving.
 struct Plan {
     size_t cache, aT, pol, pS, ctr, phys, active_sum, selcount, slot_of, slot_exp, state_total;
-    size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, zero_row, ws_total;
+    size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, zero_row, units, ws_total;
     size_t arena;
 };
+
+int max_units(const cmoe_config* c) {
+    return c->N + (int)(((int64_t)c->S * c->K + cmoe::kUnitTokens - 1) / cmoe::kUnitTokens);
+}
 
 Plan make_plan(const cmoe_config* c, const Derived& dv) {
     Plan p{};
@@ -138,6 +142,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.act = take(S * K * (size_t)c->F * dv.esz);
     p.yp = take(S * K * (size_t)c->d * 4);
     p.zero_row = take(N * 4);
+    p.units = take((size_t)max_units(c) * 4);
     p.ws_total = o;
     p.arena = L * (size_t)dv.n_slots * dv.expert_bytes;
     return p;
@@ -211,8 +216,8 @@ hipError_t timed(cmoe_handle* hd, int kid, hipStream_t st, F&& launch) {
 
 // One residency event of `layer` on stream st; advances the layer's slot-map
 // version.
-hipError_t fill(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, hipStream_t st) {
-    FillArgs f{layer, kind, hd->ver[layer], counted ? 1 : 0, zero_pre ? 1 : 0};
+hipError_t fill(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, hipStream_t st, int bbuf = -1) {
+    FillArgs f{layer, kind, hd->ver[layer], counted ? 1 : 0, zero_pre ? 1 : 0, bbuf};
     hd->ver[layer] ^= 1;
     return timed(hd, KID_FILL, st, [&] { return cmoe::launch_fill(hd->lo, f, st); });
 }
@@ -253,7 +258,8 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
         if (hd->dv.iS > 0) a.z[hd->dv.iS] = zS;
         HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "cache step");
         hd->g += 1;
-        HIPCHK(fill(hd, l, 0, counted, !refine_on, M), "fill");  // demand loads gate this layer's FFN
+        // demand loads gate this layer's FFN; the same launch lays out the FFN work units
+        HIPCHK(fill(hd, l, 0, counted, !refine_on, M, inject ? -1 : bbuf), "fill");
         if (refine_next) {
             if (hd->side_is_main) {
                 HIPCHK(fill(hd, l + 1, 1, counted, false, M), "fill");
@@ -380,6 +386,8 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.act = wb + p.act;
     lo.yp = reinterpret_cast<float*>(wb + p.yp);
     lo.zero_row = reinterpret_cast<float*>(wb + p.zero_row);
+    lo.units = reinterpret_cast<int32_t*>(wb + p.units);
+    lo.max_units = max_units(cfg);
 
     auto mk = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
     hd->ev_access.resize(cfg->L);

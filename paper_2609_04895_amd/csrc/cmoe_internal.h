@@ -15,11 +15,13 @@ constexpr int kMaxSplit = 16;        // router split-K partials per logit, at mo
 constexpr int kRouterWaves = 4;      // router: wavefronts per workgroup, one k sub-range each
 constexpr int kStreamsPerBlock = 1;   // cache-step kernel: one wavefront per stream
 constexpr int kFillBlocks = 128;  // fill kernel workgroups
+constexpr int kUnitTokens = 64;   // FFN work unit: up to 64 tokens of one expert (one pass over its weights)
 
 // Every pointer the kernels use, carved out of the caller's buffers.
 struct Layout {
     int32_t L, N, K, d, F, C, S, mode, dtype, NW, n_slots, n_r, nsplit, rdk, zstride, warmup;
     int32_t iT, iS;        // router slot of the Temporal / Spatio Router, -1 if not used
+    int32_t max_units;     // FFN work units per layer step, at most N + ceil(S K / kUnitTokens)
     int32_t policy;        // retention priority (cmoe_policy)
     float lrfu_w;          // LRFU decay per token, fl32(2^-lambda)
     int64_t expert_elems;  // 3 d F
@@ -53,6 +55,8 @@ struct Layout {
     void* act;                  // [S][K][F]   SwiGLU intermediate (dtype)
     float* yp;                  // [S][K][d]   gated expert outputs
     float* zero_row;            // [N]         zeros (native bias when there is none)
+    int32_t* units;             // [max_units] FFN work units of the layer step, heaviest
+                                //             first: expert | (pass << 16), -1 past the end
 };
 
 // cache-step kernel flags
@@ -80,6 +84,7 @@ struct FillArgs {
     int32_t rv;
     int32_t counted;
     int32_t zero_pre;    // kind 0: no refinement happened this token, clear its fill count
+    int32_t bbuf;        // kind 0: bucket buffer of the layer step (builds the FFN work units)
 };
 
 hipError_t launch_init(const Layout& lo, hipStream_t st);

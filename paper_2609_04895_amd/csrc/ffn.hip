@@ -30,7 +30,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kNG = 4;          // token groups (of 16) per pass when a bucket holds more than 16
+constexpr int kNG = 4;          // token groups (of 16) per pass when a unit holds more than 16
+static_assert(kUnitTokens == 16 * kNG, "one work unit is one pass over the weights");
 constexpr int kUnroll = 4;      // k chunks per load block, one token group
 constexpr int kUnrollWide = 2;  // k chunks per load block, kNG token groups
 
@@ -166,13 +167,19 @@ __device__ inline void up_passes(const Layout& lo, int l, int ft, const int32_t*
     }
 }
 
+// Work unit u (the fill kernel lays them out, heaviest first) = tokens
+// [kUnitTokens p, kUnitTokens (p + 1)) of expert e's bucket; workgroup
+// (u, ft) runs that pass for one 16-row F-tile.
 __global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, int bbuf, int sv, const uint16_t* __restrict__ h) {
     const int ftn = lo.F / 16;
-    const int e = blockIdx.x / ftn, ft = blockIdx.x - e * ftn;
-    const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
+    const int u = blockIdx.x / ftn, ft = blockIdx.x - u * ftn;
+    const int unit = lo.units[u];
+    if (unit < 0) return;
+    const int e = unit & 0xFFFF, t0 = kUnitTokens * (unit >> 16);
     const int slot = expert_slot(lo, l, sv, e);
-    if (m == 0 || slot < 0) return;
-    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
+    const int m = min(kUnitTokens, lo.bcount[(int64_t)bbuf * lo.N + e] - t0);
+    if (m <= 0 || slot < 0) return;
+    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S + t0;
     // packed slot layout: chunk c of this row tile is 256 units of 16 bytes,
     // gate half 0, gate half 1, up half 0, up half 1, each 64 units
     const uint4* tileA =
@@ -217,11 +224,14 @@ __device__ inline void down_passes(const Layout& lo, int l, int dt, const int32_
 
 __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l, int bbuf, int sv) {
     const int dtn = lo.d / 32;
-    const int e = blockIdx.x / dtn, dt = blockIdx.x - e * dtn;
-    const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
+    const int u = blockIdx.x / dtn, dt = blockIdx.x - u * dtn;
+    const int unit = lo.units[u];
+    if (unit < 0) return;
+    const int e = unit & 0xFFFF, t0 = kUnitTokens * (unit >> 16);
     const int slot = expert_slot(lo, l, sv, e);
-    if (m == 0 || slot < 0) return;
-    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
+    const int m = min(kUnitTokens, lo.bcount[(int64_t)bbuf * lo.N + e] - t0);
+    if (m <= 0 || slot < 0) return;
+    const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S + t0;
     // packed slot layout: after the gate/up part (F d / 4 units), chunk c of
     // this 32-row tile is 256 units: rows 0-15 half 0, half 1, rows 16-31
     // half 0, half 1, each 64 units
@@ -317,7 +327,7 @@ __global__ __launch_bounds__(64) void combine_kernel(Layout lo, int l, float* __
 
 hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st) {
     if (lo.dtype == 1)
-        hipLaunchKernelGGL(ffn_up_bf16, dim3(lo.N * (lo.F / 16)), dim3(64), 0, st, lo, l, bbuf, sv,
+        hipLaunchKernelGGL(ffn_up_bf16, dim3(lo.max_units * (lo.F / 16)), dim3(64), 0, st, lo, l, bbuf, sv,
                            static_cast<const uint16_t*>(h));
     else
         hipLaunchKernelGGL(ffn_up_f32, dim3(lo.N * (lo.F / 64)), dim3(64), 0, st, lo, l, bbuf, sv,
@@ -327,7 +337,7 @@ hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* 
 
 hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st) {
     if (lo.dtype == 1)
-        hipLaunchKernelGGL(ffn_down_bf16, dim3(lo.N * (lo.d / 32)), dim3(64), 0, st, lo, l, bbuf, sv);
+        hipLaunchKernelGGL(ffn_down_bf16, dim3(lo.max_units * (lo.d / 32)), dim3(64), 0, st, lo, l, bbuf, sv);
     else
         hipLaunchKernelGGL(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), 0, st, lo, l, bbuf, sv);
     return hipGetLastError();

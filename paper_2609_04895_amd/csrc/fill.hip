@@ -100,6 +100,10 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
     const int N = lo.N, layer = f.layer;
     const int32_t* so_in = lo.slot_of + ((int64_t)f.rv * lo.L + layer) * N;
     const int32_t* se_in = lo.slot_exp + ((int64_t)f.rv * lo.L + layer) * lo.n_slots;
+    // bucket sizes for the FFN work units (read early: the load overlaps the
+    // residency work below)
+    const bool units = f.bbuf >= 0 && blockIdx.x == 0;
+    const int m_own = (units && tid < N) ? lo.bcount[(int64_t)f.bbuf * N + tid] : 0;
     if (tid < 4) U[tid] = 0ull;
     if (tid < N) so[tid] = so_in[tid];
     if (tid < lo.n_slots) se[tid] = se_in[tid];
@@ -143,6 +147,43 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
             if (f.zero_pre) lo.step_fills[layer * 2 + 1] = 0;
             if (f.counted) lo.phys[layer * 2 + f.kind] += nenter;
         }
+    }
+    // FFN work units of this layer step: each expert's bucket cut into passes
+    // of up to kUnitTokens tokens.  When no bucket needs a second pass, unit e
+    // is expert e (or -1 if it has no tokens).
+    const bool multi = __syncthreads_or(units && m_own > kUnitTokens) != 0;
+    if (units && !multi) {
+        // blockDim.x >= N: thread e holds expert e's bucket size
+        for (int i = tid; i < lo.max_units; i += blockDim.x) lo.units[i] = (i < N && m_own > 0) ? i : -1;
+    } else if (units) {
+        // otherwise experts with more tokens go first (lower index on ties),
+        // so the longest units start first.  Rank of expert e = number of
+        // larger keys (m << 8) | (255 - e), all distinct.
+        __shared__ __align__(16) int key[kMaxN];
+        __shared__ int by_rank[kMaxN], who[kMaxN];
+        const int m = m_own;
+        const int mykey = (m << 8) | (255 - tid);
+        key[tid] = tid < N ? mykey : -1;  // blockDim.x == kMaxN: every entry is written
+        __syncthreads();
+        int rank = 0;
+        if (tid < N) {
+            const int4* k4 = reinterpret_cast<const int4*>(key);
+            for (int u = 0; u < (N + 3) / 4; ++u) {
+                const int4 v = k4[u];
+                rank += (v.x > mykey) + (v.y > mykey) + (v.z > mykey) + (v.w > mykey);
+            }
+        }
+        if (tid < N) {
+            by_rank[rank] = (m + kUnitTokens - 1) / kUnitTokens;
+            who[rank] = tid;
+        }
+        __syncthreads();
+        const int passes = tid < N ? by_rank[tid] : 0;
+        int total;
+        const int off = block_scan(passes, &total, lds4);
+        if (tid < N)
+            for (int q = 0; q < passes; ++q) lo.units[off + q] = who[tid] | (q << 16);
+        for (int i = total + tid; i < lo.max_units; i += blockDim.x) lo.units[i] = -1;
     }
     if (nenter == 0) return;
     const int64_t bytes = lo.expert_elems * (lo.dtype == 1 ? 2 : 4);
