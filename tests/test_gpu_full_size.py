@@ -39,6 +39,11 @@ def run_full(w, T, ffn_samples=8, seed=0):
               for _ in range(ffn_samples)}
     ulp_diffs = 0
     worst = 0.0
+    max_abs64 = 0.0       # max |z_gpu - z_fp64| over all sampled logits
+    max_ulp64 = 0.0       # the same in units of the fp32 ulp of z (0.5: correctly rounded)
+    near_ties = 0         # (stream, token, layer) whose K-th / (K+1)-th native logit gap is < 1e-6
+    mats = [WR] + ([WT] if w.has_temporal else []) + ([WS] if w.has_spatio else [])
+    W64 = [[M[l].astype(np.float64) for l in range(w.L)] for M in mats]
     experts = {}
     for t in range(T):
         eng.cmoe_step(inp["hidden"][t], y)
@@ -50,6 +55,20 @@ def run_full(w, T, ffn_samples=8, seed=0):
             gap = np.abs(zg.astype(np.float64) - ref)
             assert np.all(gap <= np.spacing(np.abs(ref))), f"token {t}: logit differs by more than one ulp"
             ulp_diffs += int(d.sum())
+        # fp64 logits from numpy (independent of the oracle's C code)
+        for i, s in enumerate(streams):
+            for l in range(w.L):
+                h64 = H[(s, l)][t].astype(np.float64)
+                for r in range(len(mats)):
+                    z64 = W64[r][l] @ h64
+                    if r == 0 and bias is not None:
+                        z64 = z64 + bias[l].astype(np.float64)
+                    err = np.abs(zg[i, l, r].astype(np.float64) - z64)
+                    max_abs64 = max(max_abs64, float(err.max()))
+                    max_ulp64 = max(max_ulp64, float(np.max(err / np.spacing(np.abs(z64).astype(np.float32)))))
+                    if r == 0 and w.K < w.N:
+                        zs = np.sort(z64)[::-1]
+                        near_ties += int(zs[w.K - 1] - zs[w.K] < 1e-6)
         out = run.step(*split_slots(w, zg), want="all")
         sel = eng.cmoe_read(B.CMOE_VIEW_SELECTED)                 # [L][S][K]
         assert np.array_equal(sel[:, streams].transpose(1, 0, 2), out["sel"]), f"token {t}: selections"
@@ -88,7 +107,10 @@ def run_full(w, T, ffn_samples=8, seed=0):
     assert tot["phys_fills"] <= tot["demand_misses"] + tot["proactive_loads"]
     if not w.has_spatio or w.R == 0:
         assert tot["proactive_loads"] == 0
-    say(f"{w.name}: ok; one-ulp logit differences {ulp_diffs}; worst FFN error {worst:.3g}; "
+    assert max_ulp64 <= 1.0, f"max |z_gpu - z_fp64| = {max_ulp64} ulp"
+    say(f"{w.name}: ok; one-ulp logit differences {ulp_diffs}; max |z_gpu - z_fp64| {max_abs64:.3g} "
+        f"({max_ulp64:.3f} ulp); "
+        f"Top-K near-tie opportunities (gap < 1e-6) {near_ties}; worst FFN error {worst:.3g}; "
         f"hit {1 - tot['demand_misses'] / tot['accesses']:.4f}; proactive {tot['proactive_loads']}; "
         f"physical fills {tot['phys_fills']}")
     eng.cmoe_destroy()
