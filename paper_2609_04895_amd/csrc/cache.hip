@@ -102,59 +102,37 @@ constexpr int kRowHalfMirror = 0x141;
 constexpr int kRowMirror = 0x140;
 constexpr int kRowShl1 = 0x101;     // lane i reads lane i + n of its row
 
-__device__ inline unsigned long long pack64(unsigned hi, unsigned lo) {
-    return ((unsigned long long)hi << 32) | lo;
+// maximum (MAX) or minimum of a 32-bit unsigned value over the wavefront,
+// wave-uniform
+template <bool MAX>
+__device__ inline uint32_t wave_reduce_u32(uint32_t v) {
+    auto op = [](uint32_t a, uint32_t b) { return MAX ? (a > b ? a : b) : (a < b ? a : b); };
+    v = op(v, dpp<kQuadXor1>(v));
+    v = op(v, dpp<kQuadXor2>(v));
+    v = op(v, dpp<kRowHalfMirror>(v));
+    v = op(v, dpp<kRowMirror>(v));
+    const auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    v = op(p[0], p[1]);
+    const auto q = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    v = op(q[0], q[1]);
+    return __builtin_amdgcn_readfirstlane(v);
 }
 
-template <int CTRL>
-__device__ inline unsigned long long dpp64(unsigned long long v) {
-    return pack64(dpp<CTRL>((unsigned)(v >> 32)), dpp<CTRL>((unsigned)v));
-}
-
-// {v of this lane, v of lane ^ 16} and {v of this lane, v of lane ^ 32}
-__device__ inline void swap16_64(unsigned long long v, unsigned long long& a, unsigned long long& b) {
-    const auto h = __builtin_amdgcn_permlane16_swap((unsigned)(v >> 32), (unsigned)(v >> 32), false, false);
-    const auto l = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
-    a = pack64(h[0], l[0]);
-    b = pack64(h[1], l[1]);
-}
-__device__ inline void swap32_64(unsigned long long v, unsigned long long& a, unsigned long long& b) {
-    const auto h = __builtin_amdgcn_permlane32_swap((unsigned)(v >> 32), (unsigned)(v >> 32), false, false);
-    const auto l = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
-    a = pack64(h[0], l[0]);
-    b = pack64(h[1], l[1]);
-}
-
-__device__ inline unsigned long long max64(unsigned long long a, unsigned long long b) { return a > b ? a : b; }
-__device__ inline unsigned long long min64(unsigned long long a, unsigned long long b) { return a < b ? a : b; }
-
-__device__ inline unsigned long long uniform64(unsigned long long v) {
-    return pack64(__builtin_amdgcn_readfirstlane((unsigned)(v >> 32)), __builtin_amdgcn_readfirstlane((unsigned)v));
-}
-
-// maximum over the wavefront, returned as a wave-uniform value
-__device__ inline unsigned long long wave_max_u64(unsigned long long v) {
-    v = max64(v, dpp64<kQuadXor1>(v));
-    v = max64(v, dpp64<kQuadXor2>(v));
-    v = max64(v, dpp64<kRowHalfMirror>(v));
-    v = max64(v, dpp64<kRowMirror>(v));
-    unsigned long long a, b;
-    swap16_64(v, a, b);
-    v = max64(a, b);
-    swap32_64(v, a, b);
-    return uniform64(max64(a, b));
-}
-
-__device__ inline unsigned long long wave_min_u64(unsigned long long v) {
-    v = min64(v, dpp64<kQuadXor1>(v));
-    v = min64(v, dpp64<kQuadXor2>(v));
-    v = min64(v, dpp64<kRowHalfMirror>(v));
-    v = min64(v, dpp64<kRowMirror>(v));
-    unsigned long long a, b;
-    swap16_64(v, a, b);
-    v = min64(a, b);
-    swap32_64(v, a, b);
-    return uniform64(min64(a, b));
+// The largest key (wave-uniform) and the lowest expert index e = 64 j + lane
+// holding it: a 32-bit reduction, then one ballot per register.
+template <int NPL>
+__device__ inline int argmax_lowest(const uint32_t (&key)[NPL], uint32_t& kmax) {
+    uint32_t b = key[0];
+#pragma unroll
+    for (int j = 1; j < NPL; ++j) b = key[j] > b ? key[j] : b;
+    kmax = wave_reduce_u32<true>(b);
+    int e = -1;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+        const unsigned long long bal = __ballot(key[j] == kmax);
+        if (e < 0 && bal) e = j * 64 + __builtin_ctzll(bal);
+    }
+    return e;
 }
 
 __device__ inline float wave_max_f32(float v) {
@@ -235,16 +213,24 @@ __device__ inline bool bit_of(const unsigned long long (&w)[NPL], int e) {
 template <int NPL>
 __device__ inline unsigned long long argmin_member(const float (&sc)[NPL], const unsigned long long (&member)[NPL],
                                                    int N, int lane) {
-    unsigned long long best = ~0ull;
+    uint32_t key[NPL];
+    bool in[NPL];
+    uint32_t b = 0xFFFFFFFFu;
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
         const int e = j * 64 + lane;
-        if (e < N && ((member[j] >> lane) & 1ull)) {
-            const unsigned long long k = ((unsigned long long)ord32(sc[j]) << 32) | (unsigned)e;
-            best = k < best ? k : best;
-        }
+        in[j] = e < N && ((member[j] >> lane) & 1ull);
+        key[j] = in[j] ? ord32(sc[j]) : 0xFFFFFFFFu;
+        b = key[j] < b ? key[j] : b;
     }
-    return wave_min_u64(best);
+    const uint32_t kmin = wave_reduce_u32<false>(b);
+    int e = -1;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+        const unsigned long long bal = __ballot(in[j] && key[j] == kmin);
+        if (e < 0 && bal) e = j * 64 + __builtin_ctzll(bal);
+    }
+    return e < 0 ? ~0ull : (((unsigned long long)kmin << 32) | (unsigned)e);
 }
 
 template <int NPL>
@@ -267,16 +253,16 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, int t, bool c
                            const float (&aTv)[NPL], const unsigned long long (&cw_in)[NPL], int64_t ctr_p, int lane) {
     const int N = lo.N;
     float sST[NPL];
-    unsigned long long cand[NPL];
+    uint32_t cand[NPL];  // ordered scores; 0 = not a candidate (no real score maps to 0)
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
         const int e = j * 64 + lane;
         if (e < N) {
             sST[j] = aTv[j] + pred[j];
-            cand[j] = ((unsigned long long)ord32(sST[j]) << 32) | (0xFFFFFFFFu - (unsigned)e);
+            cand[j] = ord32(sST[j]);
         } else {
             sST[j] = 0.0f;
-            cand[j] = 0ull;
+            cand[j] = 0u;
         }
     }
     unsigned long long* cptr = lo.cache + ((int64_t)s * lo.L + rl) * lo.NW;
@@ -293,15 +279,11 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, int t, bool c
     for (int j = 0; j < NPL; ++j) ins[j] = 0ull;
     const int Rn = R < N ? R : N;
     for (int i = 0; i < Rn; ++i) {
-        unsigned long long best = 0ull;
-#pragma unroll
-        for (int j = 0; j < NPL; ++j) best = cand[j] > best ? cand[j] : best;
-        best = wave_max_u64(best);
-        const int e = (int)(0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull));
-        const uint32_t ord_e = (uint32_t)(best >> 32);
+        uint32_t ord_e;
+        const int e = argmax_lowest(cand, ord_e);  // highest s^ST, lower index on ties
 #pragma unroll
         for (int j = 0; j < NPL; ++j)
-            if (cand[j] == best) cand[j] = 0ull;  // unique key: only the owner matches
+            if (j == (e >> 6) && lane == (e & 63)) cand[j] = 0u;
         if (bit_of(cw, e)) continue;              // already resident
         if (count < lo.C) {
             set_bit(cw, e);
@@ -427,11 +409,11 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
         if (NR >= 2 && spatio) softmax_fixed<NPL>(z[NR - 1], N, lane, pred);
 
         // Top-K by native logit, lower index first on ties
-        unsigned long long key[NPL];
+        uint32_t key[NPL];  // ordered native logits; 0 = taken or past N (no real logit maps to 0)
 #pragma unroll
         for (int j = 0; j < NPL; ++j) {
             const int e = j * 64 + lane;
-            key[j] = e < N ? (((unsigned long long)ord32(z[0][j]) << 32) | (0xFFFFFFFFu - (unsigned)e)) : 0ull;
+            key[j] = e < N ? ord32(z[0][j]) : 0u;
         }
         unsigned long long sw[NPL];
 #pragma unroll
@@ -439,16 +421,13 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
         float gsum = 0.0f, my_p = 0.0f;
         int my_sel = 0;
         for (int k = 0; k < K; ++k) {
-            unsigned long long best = 0ull;
-#pragma unroll
-            for (int j = 0; j < NPL; ++j) best = key[j] > best ? key[j] : best;
-            best = wave_max_u64(best);
-            const int e = (int)(0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull));
+            uint32_t kmax;
+            const int e = argmax_lowest(key, kmax);  // highest logit, lower index on ties
             float pv = 0.0f;
 #pragma unroll
             for (int j = 0; j < NPL; ++j) {
-                if (key[j] == best) {
-                    key[j] = 0ull;
+                if (j == (e >> 6) && lane == (e & 63)) {
+                    key[j] = 0u;
                     pv = pR[j];
                 }
             }

@@ -93,6 +93,9 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     int rdk = 32;
     while (splits(rdk) > cmoe::kMaxSplit) rdk *= 2;
     while (W * 2 * rdk <= c->d && tiles * W * splits(2 * rdk) >= 1024) rdk *= 2;
+    // a single partial per logit leaves big layers (many streams, three
+    // routers) with under two wavefronts per SIMD: take two
+    if (splits(rdk) == 1 && tiles * W < 2048 && rdk >= 64) rdk /= 2;
     dv->rdk = rdk;
     dv->nsplit = (int)splits(rdk);
     dv->zstride = dv->nsplit <= 4 ? 4 : cmoe::kMaxSplit;  // partial slots per logit
