@@ -105,6 +105,8 @@ def run_full(w, T, ffn_samples=8, seed=0):
     assert tot["tokens"] == w.S * T
     assert tot["traffic_bytes"] == (tot["demand_misses"] + tot["proactive_loads"]) * w.expert_bytes
     assert tot["phys_fills"] <= tot["demand_misses"] + tot["proactive_loads"]
+    if w.S == 1:   # the arena is the stream's own cache: every logical load is a copy
+        assert tot["phys_fills"] == tot["demand_misses"] + tot["proactive_loads"]
     if not w.has_spatio or w.R == 0:
         assert tot["proactive_loads"] == 0
     assert max_ulp64 <= 1.0, f"max |z_gpu - z_fp64| = {max_ulp64} ulp"
@@ -144,3 +146,10 @@ def test_full_size_qwen3_235b_slice_host_pool():
     per_layer = w.N * w.expert_bytes / 1e9
     L = min(w.L, int(0.85 * PINNED_CAP_GB // per_layer))
     run_full(w.replace(L=L), T=8, ffn_samples=4)
+
+
+def test_full_size_qwen3_30b_single_stream_pinned_pool():
+    """One decode stream at the Qwen3 shape with the cold pool in pinned host
+    memory: the HBM arena holds exactly C = 32 slots per layer (the paper's
+    per-layer capacity taken literally) and physical copies equal D + P."""
+    run_full(synth.WORKLOADS["qwen3_30b_s1"], T=12, ffn_samples=6)
