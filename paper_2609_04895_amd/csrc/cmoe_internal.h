@@ -56,7 +56,7 @@ struct Layout {
     float* yp;                  // [S][K][d]   gated expert outputs
     float* zero_row;            // [N]         zeros (native bias when there is none)
     int32_t* units;             // [max_units] FFN work units of the layer step, heaviest
-                                //             first: expert | (pass << 16), -1 past the end
+                                //             first: (pass << 8) | expert, -1 past the end
 };
 
 // cache-step kernel flags

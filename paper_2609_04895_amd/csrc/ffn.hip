@@ -175,7 +175,7 @@ __global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, int bbuf, in
     const int u = blockIdx.x / ftn, ft = blockIdx.x - u * ftn;
     const int unit = lo.units[u];
     if (unit < 0) return;
-    const int e = unit & 0xFFFF, t0 = kUnitTokens * (unit >> 16);
+    const int e = unit & 255, t0 = kUnitTokens * (unit >> 8);
     const int slot = expert_slot(lo, l, sv, e);
     const int m = min(kUnitTokens, lo.bcount[(int64_t)bbuf * lo.N + e] - t0);
     if (m <= 0 || slot < 0) return;
@@ -227,7 +227,7 @@ __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l, int bbuf, 
     const int u = blockIdx.x / dtn, dt = blockIdx.x - u * dtn;
     const int unit = lo.units[u];
     if (unit < 0) return;
-    const int e = unit & 0xFFFF, t0 = kUnitTokens * (unit >> 16);
+    const int e = unit & 255, t0 = kUnitTokens * (unit >> 8);
     const int slot = expert_slot(lo, l, sv, e);
     const int m = min(kUnitTokens, lo.bcount[(int64_t)bbuf * lo.N + e] - t0);
     if (m <= 0 || slot < 0) return;

@@ -182,7 +182,7 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
         int total;
         const int off = block_scan(passes, &total, lds4);
         if (tid < N)
-            for (int q = 0; q < passes; ++q) lo.units[off + q] = who[tid] | (q << 16);
+            for (int q = 0; q < passes; ++q) lo.units[off + q] = (q << 8) | who[tid];
         for (int i = total + tid; i < lo.max_units; i += blockDim.x) lo.units[i] = -1;
     }
     if (nenter == 0) return;

@@ -104,15 +104,16 @@ def ar1_params(w: Workload) -> Tuple[float, float]:
 
 
 def router_tid(kind: int, layer: int) -> int:
-    return (kind << 56) + layer
+    return (int(kind) << 56) + int(layer)
 
 
 def expert_tid(w: Workload, layer: int, expert: int) -> int:
-    return (KIND_EXPERT << 56) + layer * w.N + expert
+    # Python ints throughout: numpy integer indices would overflow in 64-bit ids
+    return (KIND_EXPERT << 56) + int(layer) * w.N + int(expert)
 
 
 def hidden_tid(stream: int, layer: int) -> int:
-    return (KIND_HIDDEN << 56) + (stream << 24) + layer
+    return (KIND_HIDDEN << 56) + (int(stream) << 24) + int(layer)
 
 
 # ---------------------------------------------------------------- host twin

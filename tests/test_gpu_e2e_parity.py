@@ -141,6 +141,15 @@ def test_bf16_ragged_chunks_and_zipf_bias():
     run_e2e(w, T=6, tol=2e-2)
 
 
+def test_bf16_hot_experts_span_several_ffn_units():
+    # 160 streams over 8 Zipf-biased experts: the hottest buckets hold well
+    # over 64 tokens, so they are cut into several FFN work units, ranked by
+    # size; every output is checked
+    w = synth.WORKLOADS["qwen3_30b_zipf"].replace(name="bf16_hot_units", L=2, N=8, K=2, d=256, F=128, S=160, C=4,
+                                                  R=2)
+    run_e2e(w, T=4, tol=2e-2)
+
+
 def test_bf16_update_only_gptoss_like():
     w = synth.WORKLOADS["gptoss_20b"].replace(name="gptoss_small", L=2, d=192, F=192, S=7,
                                               mode=synth.MODE_TEMPORAL, R=0)
