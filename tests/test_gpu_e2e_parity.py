@@ -150,6 +150,19 @@ def test_bf16_hot_experts_span_several_ffn_units():
     run_e2e(w, T=4, tol=2e-2)
 
 
+def test_bf16_256_experts_full_mode():
+    # four experts per lane in the cache kernel, sixteen expert tiles per router
+    w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_n256", L=2, N=256, d=256, F=128, S=10, C=40, R=6,
+                                             mode=synth.MODE_SPATIO_TEMPORAL)
+    run_e2e(w, T=5, tol=2e-2)
+
+
+def test_fp32_pool_in_pinned_host_memory():
+    # plain fp32 expert copies read from pinned host memory by the fill kernel
+    w = synth.WORKLOADS["tiny"].replace(name="tiny_host_pool", pool_kind=synth.POOL_HOST_PINNED, S=3, C=4)
+    run_e2e(w, T=24, tol=1e-5)
+
+
 def test_bf16_update_only_gptoss_like():
     w = synth.WORKLOADS["gptoss_20b"].replace(name="gptoss_small", L=2, d=192, F=192, S=7,
                                               mode=synth.MODE_TEMPORAL, R=0)
