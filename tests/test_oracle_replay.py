@@ -201,6 +201,38 @@ def test_physical_residency_is_the_union_and_fills_are_bounded():
     assert tot["phys_fills"] <= tot["demand_misses"] + tot["proactive_loads"]
 
 
+def test_slot_assignment_follows_the_lowest_free_slot_rule():
+    """Update-only mode has one residency event per (token, layer), so the
+    slot maps can be re-derived from the cache trajectory alone: a resident
+    expert keeps its slot, experts that left every cache free theirs, and each
+    newly needed expert, in ascending order, takes the lowest free slot."""
+    rng = np.random.default_rng(17)
+    L, N, K, C, T, S = 3, 16, 3, 4, 30, 3
+    zR, zT, _ = random_logits(rng, T, S, L, N)
+    run = oracle.Run(L, N, K, C, 0, S, TEMPORAL)
+    n_slots = min(N, S * C)
+    slot = [dict() for _ in range(L)]
+    fills = 0
+    for t in range(T):
+        out = run.step(zR[t], zT[t], want="all")
+        for l in range(L):
+            union = set(np.nonzero(run.cache[:, l].any(axis=0))[0].tolist())
+            for e in [e for e in slot[l] if e not in union]:
+                del slot[l][e]
+            new = sorted(union - set(slot[l]))
+            free = sorted(set(range(n_slots)) - set(slot[l].values()))
+            for e, q in zip(new, free):
+                slot[l][e] = q
+            assert len(new) <= len(free)
+            assert out["fills"][l, 0] == len(new)
+            fills += len(new)
+            want = np.full(N, -1, np.int32)
+            for e, q in slot[l].items():
+                want[e] = q
+            assert np.array_equal(run.slot_of[l], want), (t, l)
+    assert run.totals()["phys_fills"] == fills
+
+
 def test_refinement_loads_at_most_r_per_layer_step_and_starts_at_second_token():
     rng = np.random.default_rng(8)
     L, N, K, C, R, T, S = 4, 16, 2, 6, 3, 30, 2
