@@ -16,7 +16,9 @@ from typing import Optional
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# ORACLE_LIBRARY lets the planted-mistake tests load a deliberately broken
+# build of oracle.c; nothing else sets it.
+LIB_PATH = os.environ.get("ORACLE_LIBRARY") or os.path.join(_HERE, "liboracle.so")
 
 NCTR = 5  # A, hits, D, P, T
 MODE_TEMPORAL, MODE_SPATIO_TEMPORAL, MODE_SPATIO_ONLY = 0, 1, 2
