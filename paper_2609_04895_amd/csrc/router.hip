@@ -24,31 +24,78 @@ namespace cmoe {
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-__device__ inline void load8_as_f64(const void* base, int64_t idx, bool bf16, bool valid, double* out) {
-    // 8 consecutive values widened exactly to fp64
-    if (!valid) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) out[j] = 0.0;
-        return;
+// 8 consecutive values of a row as loaded (one 16-byte load for bf16, two
+// for fp32), then widened exactly to fp64.
+template <bool BF16>
+struct Raw8 {
+    uint4 v[BF16 ? 1 : 2];
+};
+
+template <bool BF16>
+__device__ inline Raw8<BF16> load8(const void* base, int64_t idx) {
+    Raw8<BF16> r;
+    if constexpr (BF16) {
+        r.v[0] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(base) + idx);
+    } else {
+        const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(base) + idx);
+        r.v[0] = p[0];
+        r.v[1] = p[1];
     }
-    if (bf16) {
-        const uint4 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(base) + idx);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    return r;
+}
+
+template <bool BF16>
+__device__ inline void widen8(const Raw8<BF16>& r, double* out) {
+    uint32_t w[8];
+    if constexpr (BF16) {
+        const uint32_t p[4] = {r.v[0].x, r.v[0].y, r.v[0].z, r.v[0].w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            out[2 * j] = (double)__uint_as_float(w[j] << 16);
-            out[2 * j + 1] = (double)__uint_as_float(w[j] & 0xFFFF0000u);
+            w[2 * j] = p[j] << 16;
+            w[2 * j + 1] = p[j] & 0xFFFF0000u;
         }
     } else {
-        const float4* p = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(base) + idx);
-        const float4 a = p[0], b = p[1];
-        out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
-        out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+        const uint32_t p[8] = {r.v[0].x, r.v[0].y, r.v[0].z, r.v[0].w, r.v[1].x, r.v[1].y, r.v[1].z, r.v[1].w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) w[j] = p[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) out[j] = (double)__uint_as_float(w[j]);
+}
+
+// Loads of chunks c0 .. c0 + KB - 1, clamped to the wavefront's last chunk
+// (the re-read of a clamped chunk is never used).
+template <bool BF16, int KB>
+__device__ inline void issue_batch(const void* W, const void* h, int64_t arow, int64_t brow, int c0, int nch,
+                                   Raw8<BF16>* ra, Raw8<BF16>* rb) {
+#pragma unroll
+    for (int u = 0; u < KB; ++u) {
+        const int c = min(c0 + u, nch - 1);
+        ra[u] = load8<BF16>(W, arow + c * 32);
+        rb[u] = load8<BF16>(h, brow + c * 32);
     }
 }
 
-// grid: x = n_r * ceil(N/16) * ceil(S/16), z = nsplit; block: kRouterWaves wavefronts
-template <bool BF16>
+// Widening and matrix-core work of the chunks of a batch that lie in range,
+// in ascending k order (a wavefront-uniform test).
+template <bool BF16, int KB>
+__device__ inline void mfma_batch(const Raw8<BF16>* ra, const Raw8<BF16>* rb, int c0, int nch, f64x4& acc) {
+#pragma unroll
+    for (int u = 0; u < KB; ++u) {
+        if (c0 + u < nch) {
+            double av[8], bv[8];
+            widen8<BF16>(ra[u], av);
+            widen8<BF16>(rb[u], bv);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[j], bv[j], acc, 0, 0, 0);
+        }
+    }
+}
+
+// grid: x = n_r * ceil(N/16) * ceil(S/16), z = nsplit; block: kRouterWaves
+// wavefronts; KB = k chunks whose loads are issued together (at most the
+// chunks of a wavefront's range)
+template <bool BF16, int KB>
 __global__ __launch_bounds__(64 * kRouterWaves) void router_kernel(Layout lo, int l, const void* h, int dk) {
     __shared__ f64x4 red[kRouterWaves - 1][64];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -70,20 +117,16 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_kernel(Layout lo, in
     const int64_t arow = ((int64_t)l * lo.N + (va ? e_a : 0)) * lo.d + i0 + 8 * g;
     const int64_t brow = ((int64_t)(vb ? s_b : 0) * lo.L + l) * lo.d + i0 + 8 * g;
 
+    // Every load of a batch is issued before the first is used.  Rows past N
+    // or S read row 0: they only feed output rows and columns that are never
+    // stored.
+    const int nchu = __builtin_amdgcn_readfirstlane(nch);
     f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-    constexpr int kBatch = 4;  // chunks whose loads are issued together
-    for (int c0 = 0; c0 < nch; c0 += kBatch) {
-        double av[kBatch][8], bv[kBatch][8];
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const bool in = c0 + u < nch;
-            load8_as_f64(W, arow + (c0 + u) * 32, BF16, va && in, av[u]);
-            load8_as_f64(h, brow + (c0 + u) * 32, BF16, vb && in, bv[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u)
-#pragma unroll
-            for (int j = 0; j < 8; ++j) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[u][j], bv[u][j], acc, 0, 0, 0);
+    for (int c0 = 0; c0 < nchu; c0 += KB) {
+        Raw8<BF16> ra[KB], rb[KB];
+        issue_batch<BF16, KB>(W, h, arow, brow, c0, nchu, ra, rb);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_batch<BF16, KB>(ra, rb, c0, nchu, acc);
     }
     // the workgroup's sub-range tiles, added in wavefront order
     if (wv > 0) red[wv - 1][lane] = acc;
@@ -111,15 +154,25 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_kernel(Layout lo, in
     }
 }
 
-hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st) {
+template <bool BF16>
+static void launch_router_t(const Layout& lo, int l, const void* h, hipStream_t st) {
     const int dk = lo.rdk;  // multiple of 32; the last split may be shorter (d % 32 == 0)
-    const int tiles = lo.n_r * ((lo.N + 15) / 16) * ((lo.S + 15) / 16);
-    if (lo.dtype == 1)
-        hipLaunchKernelGGL(router_kernel<true>, dim3(tiles, 1, lo.nsplit), dim3(64 * kRouterWaves), 0, st, lo, l, h,
-                           dk);
+    const dim3 grid(lo.n_r * ((lo.N + 15) / 16) * ((lo.S + 15) / 16), 1, lo.nsplit);
+    const dim3 block(64 * kRouterWaves);
+    const int cpw = dk / 32;  // k chunks per wavefront
+    if (cpw >= 4)
+        hipLaunchKernelGGL((router_kernel<BF16, 4>), grid, block, 0, st, lo, l, h, dk);
+    else if (cpw >= 2)
+        hipLaunchKernelGGL((router_kernel<BF16, 2>), grid, block, 0, st, lo, l, h, dk);
     else
-        hipLaunchKernelGGL(router_kernel<false>, dim3(tiles, 1, lo.nsplit), dim3(64 * kRouterWaves), 0, st, lo, l, h,
-                           dk);
+        hipLaunchKernelGGL((router_kernel<BF16, 1>), grid, block, 0, st, lo, l, h, dk);
+}
+
+hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st) {
+    if (lo.dtype == 1)
+        launch_router_t<true>(lo, l, h, st);
+    else
+        launch_router_t<false>(lo, l, h, st);
     return hipGetLastError();
 }
 
