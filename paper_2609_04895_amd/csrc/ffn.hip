@@ -299,26 +299,27 @@ __global__ __launch_bounds__(64) void combine_kernel(Layout lo, int l, float* __
     if (idx >= (int64_t)lo.S * n4) return;
     const int s = (int)(idx / n4), c = (int)(idx - (int64_t)s * n4);
     const float4* yp = reinterpret_cast<const float4*>(lo.yp) + (int64_t)s * lo.K * n4 + c;
-    float4 acc = yp[0];
-    int k = 1;
-    for (; k + 8 <= lo.K; k += 8) {  // loads first, then the adds in k order
+    // Batches of 8 outputs: every load of a batch (indices clamped to K - 1;
+    // a clamped re-read is not added) is issued before the adds, which run
+    // in k order.
+    const int K = lo.K;
+    float4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < K; k0 += 8) {
         float4 v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = yp[(int64_t)(k + u) * n4];
+        for (int u = 0; u < 8; ++u) v[u] = yp[(int64_t)min(k0 + u, K - 1) * n4];
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-            acc.x = acc.x + v[u].x;
-            acc.y = acc.y + v[u].y;
-            acc.z = acc.z + v[u].z;
-            acc.w = acc.w + v[u].w;
+            if (k0 + u == 0) {
+                acc = v[0];
+            } else if (k0 + u < K) {
+                acc.x = acc.x + v[u].x;
+                acc.y = acc.y + v[u].y;
+                acc.z = acc.z + v[u].z;
+                acc.w = acc.w + v[u].w;
+            }
         }
-    }
-    for (; k < lo.K; ++k) {
-        const float4 v = yp[(int64_t)k * n4];
-        acc.x = acc.x + v.x;
-        acc.y = acc.y + v.y;
-        acc.z = acc.z + v.z;
-        acc.w = acc.w + v.w;
     }
     reinterpret_cast<float4*>(y + ((int64_t)s * lo.L + l) * lo.d)[c] = acc;
 }

@@ -93,6 +93,12 @@ __device__ inline int packed_dest_in_block(int w) {
     return (j & 1) * 64 + r + 16 * (j >> 1);
 }
 
+// Cache word i = s NW + j: word j of stream s's membership bits of the layer.
+__device__ inline unsigned long long cache_word(const Layout& lo, int layer, int i) {
+    const int s = i / lo.NW, j = i - s * lo.NW;
+    return lo.cache[((int64_t)s * lo.L + layer) * lo.NW + j];
+}
+
 __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
     __shared__ unsigned long long U[4];
     __shared__ int so[kMaxN], se[kMaxN], free_list[kMaxN], enter_list[kMaxN], lds4[4];
@@ -100,18 +106,36 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
     const int N = lo.N, layer = f.layer;
     const int32_t* so_in = lo.slot_of + ((int64_t)f.rv * lo.L + layer) * N;
     const int32_t* se_in = lo.slot_exp + ((int64_t)f.rv * lo.L + layer) * lo.n_slots;
-    // bucket sizes for the FFN work units (read early: the load overlaps the
-    // residency work below)
+    // Every global load of the prologue is issued before the first is used:
+    // the slot maps, the bucket sizes for the FFN work units and the first
+    // batch of cache words (indices clamped; a clamped value is not used).
     const bool units = f.bbuf >= 0 && blockIdx.x == 0;
-    const int m_own = (units && tid < N) ? lo.bcount[(int64_t)f.bbuf * N + tid] : 0;
+    const int S_NW = lo.S * lo.NW;
+    const int so_v = so_in[min(tid, N - 1)];
+    const int se_v = se_in[min(tid, lo.n_slots - 1)];
+    const int m_v = lo.bcount[(int64_t)max(f.bbuf, 0) * N + min(tid, N - 1)];
+    constexpr int kWords = 4;  // cache words per thread per batch
+    unsigned long long w[kWords];
+#pragma unroll
+    for (int u = 0; u < kWords; ++u) w[u] = cache_word(lo, layer, min(tid + u * (int)blockDim.x, S_NW - 1));
+    __builtin_amdgcn_sched_barrier(0);
+    const int m_own = (units && tid < N) ? m_v : 0;
     if (tid < 4) U[tid] = 0ull;
-    if (tid < N) so[tid] = so_in[tid];
-    if (tid < lo.n_slots) se[tid] = se_in[tid];
+    if (tid < N) so[tid] = so_v;
+    if (tid < lo.n_slots) se[tid] = se_v;
     __syncthreads();
-    for (int i = tid; i < lo.S * lo.NW; i += blockDim.x) {
-        const int s = i / lo.NW, j = i - s * lo.NW;
-        const unsigned long long w = lo.cache[((int64_t)s * lo.L + layer) * lo.NW + j];
-        if (w) atomicOr(&U[j], w);
+    for (int i0 = 0; i0 < S_NW; i0 += kWords * blockDim.x) {
+        if (i0 > 0) {
+#pragma unroll
+            for (int u = 0; u < kWords; ++u)
+                w[u] = cache_word(lo, layer, min(i0 + tid + u * (int)blockDim.x, S_NW - 1));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int u = 0; u < kWords; ++u) {
+            const int i = i0 + tid + u * blockDim.x;
+            if (i < S_NW && w[u]) atomicOr(&U[i % lo.NW], w[u]);
+        }
     }
     __syncthreads();
     const int e = tid;

@@ -167,3 +167,10 @@ def test_bf16_update_only_gptoss_like():
     w = synth.WORKLOADS["gptoss_20b"].replace(name="gptoss_small", L=2, d=192, F=192, S=7,
                                               mode=synth.MODE_TEMPORAL, R=0)
     run_e2e(w, T=8, tol=2e-2)
+
+
+def test_bf16_top11_output_combine():
+    # K = 11: the output combine adds a full batch of eight gated outputs and
+    # a clamped batch of three, in k order
+    w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_top11", L=2, N=32, K=11, d=128, F=64, S=12, C=16)
+    run_e2e(w, T=6, tol=2e-2)
