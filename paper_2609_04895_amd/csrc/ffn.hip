@@ -11,8 +11,10 @@
 // (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  The expert's tokens form the
 // 16 columns of the B operand (groups of 16 tokens; several groups reuse the
 // loaded weights).  Per 64-wide k chunk, lane (r, g) of the A operand holds
-// W[row r][kc + 16 g .. + 16]; the two MFMAs of a chunk take k-slots
-// kc + 16 g + {0..7} and kc + 16 g + {8..15}, the same for both operands.
+// W[row r][kc + 8 g .. + 8] and W[row r][kc + 32 + 8 g .. + 8]; the two MFMAs
+// of a chunk take k-slots kc + 8 g + {0..7} and kc + 32 + 8 g + {0..7}, the
+// same for both operands.  Each activation load thus reads one contiguous
+// 64-byte half of a token's 128-byte k chunk.
 // The weights come from the expert's HBM slot in packed order (the fill
 // kernel writes it so): each A operand load of a wavefront reads one
 // contiguous kilobyte and each wavefront streams one contiguous block.  The
@@ -101,7 +103,7 @@ __device__ inline void mfma_block(const uint4* __restrict__ tile, int c, const u
         for (int i = 0; i < U; ++i) {
             const int kc = (c + i) * 64;
             X[q][i][0] = *reinterpret_cast<const uint4*>(xb[q] + kc);
-            X[q][i][1] = *reinterpret_cast<const uint4*>(xb[q] + kc + 8);
+            X[q][i][1] = *reinterpret_cast<const uint4*>(xb[q] + kc + 32);
         }
     }
     __builtin_amdgcn_sched_barrier(0);  // keep every load of the block ahead of the matrix-core work
@@ -147,7 +149,7 @@ __device__ inline void up_passes(const Layout& lo, int l, int ft, const int32_t*
 #pragma unroll
         for (int q = 0; q < NG; ++q) pr[q] = bk[min(t0 + 16 * q + r, m - 1)];
 #pragma unroll
-        for (int q = 0; q < NG; ++q) xb[q] = h + ((int64_t)(pr[q] >> 8) * lo.L + l) * d + 16 * g;
+        for (int q = 0; q < NG; ++q) xb[q] = h + ((int64_t)(pr[q] >> 8) * lo.L + l) * d + 8 * g;
         f32x4 cg[NG], cu[NG];
         mfma_pass<NG, U>(tileA, d / 64, xb, cg, cu);
         // D[i][j]: row i = 4 g + rr of this 16-row tile, token column j = r
@@ -203,7 +205,7 @@ __device__ inline void down_passes(const Layout& lo, int l, int dt, const int32_
 #pragma unroll
         for (int q = 0; q < NG; ++q) pr[q] = bk[min(t0 + 16 * q + r, m - 1)];
 #pragma unroll
-        for (int q = 0; q < NG; ++q) xb[q] = act + ((int64_t)(pr[q] >> 8) * lo.K + (pr[q] & 255)) * F + 16 * g;
+        for (int q = 0; q < NG; ++q) xb[q] = act + ((int64_t)(pr[q] >> 8) * lo.K + (pr[q] & 255)) * F + 8 * g;
         f32x4 c0[NG], c1[NG];
         mfma_pass<NG, U>(tileB, F / 64, xb, c0, c1);
 #pragma unroll

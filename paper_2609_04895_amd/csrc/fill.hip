@@ -47,11 +47,11 @@ __device__ int block_scan(int v, int* total, int* lds4) {
 // a 64-unit run.
 //   gate/up part, units [0, F d / 4):
 //     ((((ft * (d/64) + c) * 2 + mat) * 2 + half) * 64 + lane)
-//     = W_mat[16 ft + lane % 16][64 c + 16 (lane / 16) + 8 half .. + 8],
+//     = W_mat[16 ft + lane % 16][64 c + 32 half + 8 (lane / 16) .. + 8],
 //     mat 0 = gate, 1 = up
 //   down part, units [F d / 4, 3 F d / 8):
 //     F d / 4 + ((((dt * (F/64) + c) * 2 + mt) * 2 + half) * 64 + lane)
-//     = W_down[32 dt + 16 mt + lane % 16][64 c + 16 (lane / 16) + 8 half .. + 8]
+//     = W_down[32 dt + 16 mt + lane % 16][64 c + 32 half + 8 (lane / 16) .. + 8]
 // The cold pool keeps the plain row-major layout.  Every 128-unit block of
 // the packed order (one run for each half) holds 16 source rows x 128
 // contiguous bytes: rows 16 ft + r of W_mat at columns 64 c .. 64 c + 63 for
@@ -87,10 +87,10 @@ __device__ inline BlockMap packed_block(int b, int d, int F) {
 }
 
 // Source unit w of a block (row w / 8, 16-byte chunk w % 8 of the row's 128
-// bytes) goes to packed unit (chunk % 2) * 64 + row + 16 (chunk / 2).
+// bytes) goes to packed unit (chunk / 4) * 64 + row + 16 (chunk % 4).
 __device__ inline int packed_dest_in_block(int w) {
     const int r = w >> 3, j = w & 7;
-    return (j & 1) * 64 + r + 16 * (j >> 1);
+    return (j >> 2) * 64 + r + 16 * (j & 3);
 }
 
 // Cache word i = s NW + j: word j of stream s's membership bits of the layer.

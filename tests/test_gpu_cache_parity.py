@@ -155,14 +155,14 @@ def packed_from_plain(plain_u16, d, F):
             for mat in (Wg, Wu):
                 for half in range(2):
                     for lane in range(64):
-                        row, col = 16 * ft + lane % 16, 64 * c + 16 * (lane // 16) + 8 * half
+                        row, col = 16 * ft + lane % 16, 64 * c + 32 * half + 8 * (lane // 16)
                         units.append(mat[row, col:col + 8])
     for dt in range(d // 32):
         for c in range(F // 64):
             for mt in range(2):
                 for half in range(2):
                     for lane in range(64):
-                        row, col = 32 * dt + 16 * mt + lane % 16, 64 * c + 16 * (lane // 16) + 8 * half
+                        row, col = 32 * dt + 16 * mt + lane % 16, 64 * c + 32 * half + 8 * (lane // 16)
                         units.append(Wd[row, col:col + 8])
     return np.concatenate(units)
 
