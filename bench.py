@@ -195,6 +195,9 @@ def main():
     ap.add_argument("--layers", type=int, default=None,
                     help="run the first L layers only (a pinned-host pool larger than the host allows)")
     ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
+    ap.add_argument("--ffn-shape", choices=["auto", "single", "grouped"], default="auto",
+                    help="bf16 FFN workgroups: one wavefront each, or four sharing big units' activations "
+                         "(auto: the library's choice from the average tokens per expert)")
     ap.add_argument("--no-profile", action="store_true", help="no per-kernel HIP events in the timed region")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
     ap.add_argument("--overlap-study", action="store_true",
@@ -238,7 +241,7 @@ def main():
     t0 = time.time()
     inputs = synth.device_inputs(w, T=T_gen)
     print(f"[bench] inputs generated on the device in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
-    eng = engine_for(w, inputs, warmup_tokens=warmup, side_stream=not args.fill_on_main)
+    eng = engine_for(w, inputs, warmup_tokens=warmup, side_stream=not args.fill_on_main, ffn_shape=args.ffn_shape)
     hidden = inputs["hidden"]
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
     main_stream = eng.main_stream
@@ -287,7 +290,7 @@ def main():
                    "capacity": w.C, "refine_budget": w.R if w.has_spatio else 0,
                    "mode": {0: "update-only", 1: "spatio-temporal", 2: "spatio-only"}[w.mode],
                    "retention": {v: k for k, v in POLICIES.items()}[w.policy], "d": w.d, "F": w.F,
-                   "fills": "main stream" if args.fill_on_main else "side stream"},
+                   "fills": "main stream" if args.fill_on_main else "side stream", "ffn_shape": args.ffn_shape},
     }
     # algorithmic bytes of one token step: each distinct selected expert read
     # once, router weights, hidden states in, layer outputs out, fills (read +

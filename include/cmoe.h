@@ -94,6 +94,14 @@ typedef enum {
 #define CMOE_FLAG_FILL_ON_MAIN 0x1u /* run proactive fills on the main stream too
                                        (demand fills always run there: they gate
                                        the layer's FFN)                          */
+/* bf16 expert FFN launch shape.  Single: one wavefront per workgroup, each on
+ * its own row tile.  Grouped: four wavefronts per workgroup on consecutive row
+ * tiles of one work unit; units of more than 16 tokens load their activations
+ * once per workgroup into LDS.  Default: grouped when S K >= 8 N (at least 8
+ * tokens per expert on average), else single.  Both flags: CMOE_ERR_INVALID_ARG.
+ * The results are the same either way. */
+#define CMOE_FLAG_FFN_GROUPED 0x2u
+#define CMOE_FLAG_FFN_SINGLE 0x4u
 
 /* Problem shape.  Valid values: 1 <= K <= C <= N (Section 2: capacity at least
  * Top-K); 0 <= R <= N; L, S >= 1; d, F >= 1; warmup_tokens >= 0; a known mode

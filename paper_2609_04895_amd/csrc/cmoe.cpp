@@ -45,6 +45,7 @@ enum KernelId { KID_ROUTER = 0, KID_CACHE = 1, KID_FILL = 2, KID_UP = 3, KID_DOW
 struct Derived {
     int NW, n_r, n_slots, nsplit, rdk, zstride;
     int iT, iS;        // router slots of the Temporal / Spatio Router, -1 if not used
+    int ffn_waves;     // wavefronts per bf16 FFN workgroup (1 or 4)
     size_t esz, expert_bytes;
 };
 
@@ -75,6 +76,13 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     if (c->K > cmoe::kMaxK) return fail(CMOE_ERR_UNSUPPORTED, "K > 64 is not supported");
     if (c->d % 64 || c->F % 64) return fail(CMOE_ERR_UNSUPPORTED, "d and F must be multiples of 64");
     if ((int64_t)c->S * c->K >= (int64_t)1 << 23) return fail(CMOE_ERR_UNSUPPORTED, "S*K too large");
+    if ((c->flags & CMOE_FLAG_FFN_GROUPED) && (c->flags & CMOE_FLAG_FFN_SINGLE))
+        return fail(CMOE_ERR_INVALID_ARG, "CMOE_FLAG_FFN_GROUPED and CMOE_FLAG_FFN_SINGLE exclude each other");
+    // grouped FFN workgroups pay off when buckets of more than 16 tokens are
+    // common: by default, from 8 tokens per expert on average
+    dv->ffn_waves = (c->flags & CMOE_FLAG_FFN_GROUPED) ? 4
+                    : (c->flags & CMOE_FLAG_FFN_SINGLE) ? 1
+                    : ((int64_t)c->S * c->K >= (int64_t)8 * c->N ? 4 : 1);
     dv->NW = (c->N + 63) / 64;
     const bool temporal = c->policy == CMOE_POLICY_ROUTER;
     dv->iT = temporal ? 1 : -1;
@@ -391,6 +399,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.zero_row = reinterpret_cast<float*>(wb + p.zero_row);
     lo.units = reinterpret_cast<int32_t*>(wb + p.units);
     lo.max_units = max_units(cfg);
+    lo.ffn_waves = dv.ffn_waves;
 
     auto mk = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
     hd->ev_access.resize(cfg->L);

@@ -22,6 +22,8 @@ struct Layout {
     int32_t L, N, K, d, F, C, S, mode, dtype, NW, n_slots, n_r, nsplit, rdk, zstride, warmup;
     int32_t iT, iS;        // router slot of the Temporal / Spatio Router, -1 if not used
     int32_t max_units;     // FFN work units per layer step, at most N + ceil(S K / kUnitTokens)
+    int32_t ffn_waves;     // wavefronts per bf16 FFN workgroup: 1, or 4 (grouped: units of more
+                           // than 16 tokens share their activations through LDS)
     int32_t policy;        // retention priority (cmoe_policy)
     float lrfu_w;          // LRFU decay per token, fl32(2^-lambda)
     int64_t expert_elems;  // 3 d F

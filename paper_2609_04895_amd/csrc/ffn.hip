@@ -36,6 +36,7 @@ constexpr int kNG = 4;          // token groups (of 16) per pass when a unit hol
 static_assert(kUnitTokens == 16 * kNG, "one work unit is one pass over the weights");
 constexpr int kUnroll = 4;      // k chunks per load block, one token group
 constexpr int kUnrollWide = 2;  // k chunks per load block, kNG token groups
+constexpr int kWaves = 4;       // wavefronts per grouped workgroup: consecutive row tiles of one work unit
 
 __device__ inline bf16x8 as_bf16x8(uint4 v) {
     bf16x8 r;
@@ -133,6 +134,99 @@ __device__ inline void mfma_pass(const uint4* __restrict__ tile, int nchunk, con
     for (; c < nchunk; ++c) mfma_block<NG, 1>(tile, c, xb, acc0, acc1);
 }
 
+// Grouped launch, units of more than 16 tokens: the kWaves wavefronts of a
+// workgroup (row tiles of the same unit) load the activations of each block
+// of U k-chunks from global memory once, into LDS, and read their B
+// fragments from there.
+// Slot (group q, chunk i, half hh) of a buffer holds, for lane (r, g), token
+// column r's 8 values at k = 64 (c + i) + 32 hh + 8 g.  Two buffers: one
+// barrier per block.
+template <int U>
+struct HeavyLds {
+    uint4 x[2][kNG * U * 2][64];
+};
+static_assert(kWaves == 4, "the staging split below assumes 4 wavefronts");
+
+// Staging loads of thread tid (U = 2): group q, chunk tid / 128, half
+// (tid / 64) % 2, lane tid % 64 for every q, whose token row and k offset are
+// the thread's own xb[q] (a chunk past the end is clamped; it is never used).
+struct Staged {
+    uint4 v[kNG];
+};
+
+template <int U>
+__device__ inline Staged stage_load(const uint16_t* const* xb, int c, int nchunk, int tid) {
+    static_assert(U == 2, "the staging split assumes two chunks per block");
+    const int i = tid >> 7, hh = (tid >> 6) & 1;
+    const int off = min(c + i, nchunk - 1) * 64 + 32 * hh;
+    Staged st;
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) st.v[q] = *reinterpret_cast<const uint4*>(xb[q] + off);
+    return st;
+}
+
+template <int U>
+__device__ inline void stage_store(uint4 (*xs)[64], int tid, const Staged& st) {
+    const int i = tid >> 7, hh = (tid >> 6) & 1;
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) xs[(q * U + i) * 2 + hh][tid & 63] = st.v[q];
+}
+
+// One pass of kNG token groups over a 16-row (gate/up) or 2 x 16-row (down)
+// weight tile with the activations shared through LDS.  Every wavefront of
+// the workgroup runs the loop (and its barriers); `active` wavefronts also
+// load their weights and run the matrix-core work.
+template <int U>
+__device__ inline void mfma_pass_shared(const uint4* __restrict__ tile, int nchunk, const uint16_t* const* xb,
+                                        bool active, HeavyLds<U>& sm, int tid, f32x4* acc0, f32x4* acc1) {
+    const int lane = tid & 63;
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) {
+        acc0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    // The activations of block c + U are loaded while block c computes;
+    // their LDS stores then wait only for them, not for the weight loads
+    // issued after them.
+    Staged st = stage_load<U>(xb, 0, nchunk, tid);
+    int b = 0;
+    for (int c = 0; c < nchunk; c += U, b ^= 1) {
+        uint4 A[U][4];
+        if (active) {
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+                const uint4* ch = tile + (int64_t)min(c + i, nchunk - 1) * 256;
+                A[i][0] = load_stream(ch);
+                A[i][1] = load_stream(ch + 64);
+                A[i][2] = load_stream(ch + 128);
+                A[i][3] = load_stream(ch + 192);
+            }
+        }
+        stage_store<U>(sm.x[b], tid, st);
+        __syncthreads();
+        st = stage_load<U>(xb, c + U, nchunk, tid);
+        if (!active) continue;
+#pragma unroll
+        for (int q = 0; q < kNG; ++q) {
+            uint4 X[U][2];
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+                X[i][0] = sm.x[b][(q * U + i) * 2][lane];
+                X[i][1] = sm.x[b][(q * U + i) * 2 + 1][lane];
+            }
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+                if (c + i < nchunk) {
+                    acc0[q] = mfma_bf16(A[i][0], X[i][0], acc0[q]);
+                    acc0[q] = mfma_bf16(A[i][1], X[i][1], acc0[q]);
+                    acc1[q] = mfma_bf16(A[i][2], X[i][0], acc1[q]);
+                    acc1[q] = mfma_bf16(A[i][3], X[i][1], acc1[q]);
+                }
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- bf16
 // Token groups of one pass over the weights: one group (up to 16 tokens, the
 // common case) with a deep k block, or kNG groups with a shallower one.
@@ -169,12 +263,48 @@ __device__ inline void up_passes(const Layout& lo, int l, int ft, const int32_t*
     }
 }
 
+// A unit of 17 to kUnitTokens tokens: one pass with the activations shared
+// by the workgroup.
+__device__ inline void up_heavy(const Layout& lo, int l, int ft, const int32_t* __restrict__ bk, int m,
+                                const uint4* __restrict__ tileA, const uint16_t* __restrict__ h, int tid,
+                                HeavyLds<kUnrollWide>& sm) {
+    const int lane = tid & 63, r = lane & 15, g = lane >> 4;
+    const int d = lo.d;
+    uint16_t* act = reinterpret_cast<uint16_t*>(lo.act);
+    int pr[kNG];
+    const uint16_t* xb[kNG];
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) pr[q] = bk[min(16 * q + r, m - 1)];
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) xb[q] = h + ((int64_t)(pr[q] >> 8) * lo.L + l) * d + 8 * g;
+    f32x4 cg[kNG], cu[kNG];
+    mfma_pass_shared<kUnrollWide>(tileA, d / 64, xb, true, sm, tid, cg, cu);
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) {
+        const int tok = 16 * q + r;
+        if (tok < m) {
+            uint2 o;
+            o.x = pack_bf16x2(silu_mul(cg[q][0], cu[q][0]), silu_mul(cg[q][1], cu[q][1]));
+            o.y = pack_bf16x2(silu_mul(cg[q][2], cu[q][2]), silu_mul(cg[q][3], cu[q][3]));
+            const int pair = pr[q];
+            const int64_t row = (int64_t)(pair >> 8) * lo.K + (pair & 255);
+            *reinterpret_cast<uint2*>(act + row * lo.F + ft * 16 + 4 * g) = o;
+        }
+    }
+}
+
 // Work unit u (the fill kernel lays them out, heaviest first) = tokens
 // [kUnitTokens p, kUnitTokens (p + 1)) of expert e's bucket; workgroup
-// (u, ft) runs that pass for one 16-row F-tile.
-__global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, int bbuf, int sv, const uint16_t* __restrict__ h) {
-    const int ftn = lo.F / 16;
-    const int u = blockIdx.x / ftn, ft = blockIdx.x - u * ftn;
+// (u, j) runs that pass for the W 16-row F-tiles W j + wavefront (F is a
+// multiple of 64, so every wavefront has a tile).  W = 1: every wavefront
+// on its own; W = kWaves: grouped.
+template <int W>
+__global__ __launch_bounds__(64 * W) void ffn_up_bf16(Layout lo, int l, int bbuf, int sv,
+                                                      const uint16_t* __restrict__ h) {
+    const int wgn = lo.F / (16 * W);
+    const int u = blockIdx.x / wgn;
+    const int lane = threadIdx.x & 63;
+    const int ft = (blockIdx.x - u * wgn) * W + (threadIdx.x >> 6);
     const int unit = lo.units[u];
     if (unit < 0) return;
     const int e = unit & 255, t0 = kUnitTokens * (unit >> 8);
@@ -185,11 +315,15 @@ __global__ __launch_bounds__(64) void ffn_up_bf16(Layout lo, int l, int bbuf, in
     // packed slot layout: chunk c of this row tile is 256 units of 16 bytes,
     // gate half 0, gate half 1, up half 0, up half 1, each 64 units
     const uint4* tileA =
-        reinterpret_cast<const uint4*>(slot_base(lo, l, slot)) + (int64_t)ft * (lo.d / 64) * 256 + threadIdx.x;
-    if (m <= 16)
-        up_passes<1, kUnroll>(lo, l, ft, bk, m, tileA, h, threadIdx.x);
-    else
-        up_passes<kNG, kUnrollWide>(lo, l, ft, bk, m, tileA, h, threadIdx.x);
+        reinterpret_cast<const uint4*>(slot_base(lo, l, slot)) + (int64_t)ft * (lo.d / 64) * 256 + lane;
+    if (m <= 16) {  // workgroup-uniform
+        up_passes<1, kUnroll>(lo, l, ft, bk, m, tileA, h, lane);
+    } else if constexpr (W == 1) {
+        up_passes<kNG, kUnrollWide>(lo, l, ft, bk, m, tileA, h, lane);
+    } else {
+        __shared__ HeavyLds<kUnrollWide> sm;
+        up_heavy(lo, l, ft, bk, m, tileA, h, threadIdx.x, sm);
+    }
 }
 
 template <int NG, int U>
@@ -224,9 +358,47 @@ __device__ inline void down_passes(const Layout& lo, int l, int dt, const int32_
     }
 }
 
-__global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l, int bbuf, int sv) {
+// A unit of 17 to kUnitTokens tokens in the grouped launch: one pass with
+// the SwiGLU intermediate shared by the workgroup.  Wavefronts past the last
+// d-tile (d not a multiple of 32 W) take part in the staging and barriers
+// only.
+__device__ inline void down_heavy(const Layout& lo, int l, int dt, bool active, const int32_t* __restrict__ bk, int m,
+                                  const uint4* __restrict__ tileB, int tid, HeavyLds<kUnrollWide>& sm) {
+    const int lane = tid & 63, r = lane & 15, g = lane >> 4;
+    const int F = lo.F;
+    const uint16_t* act = reinterpret_cast<const uint16_t*>(lo.act);
+    int pr[kNG];
+    const uint16_t* xb[kNG];
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) pr[q] = bk[min(16 * q + r, m - 1)];
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) xb[q] = act + ((int64_t)(pr[q] >> 8) * lo.K + (pr[q] & 255)) * F + 8 * g;
+    f32x4 c0[kNG], c1[kNG];
+    mfma_pass_shared<kUnrollWide>(tileB, F / 64, xb, active, sm, tid, c0, c1);
+    if (!active) return;
+#pragma unroll
+    for (int q = 0; q < kNG; ++q) {
+        const int tok = 16 * q + r;
+        if (tok < m) {
+            const int s = pr[q] >> 8, k = pr[q] & 255;
+            const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
+            float* dst = lo.yp + ((int64_t)s * lo.K + k) * lo.d + dt * 32 + 4 * g;
+            *reinterpret_cast<float4*>(dst) = make_float4(gk * c0[q][0], gk * c0[q][1], gk * c0[q][2], gk * c0[q][3]);
+            *reinterpret_cast<float4*>(dst + 16) =
+                make_float4(gk * c1[q][0], gk * c1[q][1], gk * c1[q][2], gk * c1[q][3]);
+        }
+    }
+}
+
+// Workgroup (u, j): the W 32-row d-tiles W j + wavefront of unit u.
+template <int W>
+__global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bbuf, int sv) {
     const int dtn = lo.d / 32;
-    const int u = blockIdx.x / dtn, dt = blockIdx.x - u * dtn;
+    const int wgn = (dtn + W - 1) / W;
+    const int u = blockIdx.x / wgn;
+    const int lane = threadIdx.x & 63;
+    const int dt = (blockIdx.x - u * wgn) * W + (threadIdx.x >> 6);
+    const bool active = dt < dtn;
     const int unit = lo.units[u];
     if (unit < 0) return;
     const int e = unit & 255, t0 = kUnitTokens * (unit >> 8);
@@ -238,11 +410,15 @@ __global__ __launch_bounds__(64) void ffn_down_bf16(Layout lo, int l, int bbuf, 
     // this 32-row tile is 256 units: rows 0-15 half 0, half 1, rows 16-31
     // half 0, half 1, each 64 units
     const uint4* tileB = reinterpret_cast<const uint4*>(slot_base(lo, l, slot)) + (int64_t)lo.F * lo.d / 4 +
-                         (int64_t)dt * (lo.F / 64) * 256 + threadIdx.x;
-    if (m <= 16)
-        down_passes<1, kUnroll>(lo, l, dt, bk, m, tileB, threadIdx.x);
-    else
-        down_passes<kNG, kUnrollWide>(lo, l, dt, bk, m, tileB, threadIdx.x);
+                         (int64_t)(active ? dt : 0) * (lo.F / 64) * 256 + lane;
+    if (m <= 16) {  // workgroup-uniform; this path has no barriers
+        if (active) down_passes<1, kUnroll>(lo, l, dt, bk, m, tileB, lane);
+    } else if constexpr (W == 1) {
+        down_passes<kNG, kUnrollWide>(lo, l, dt, bk, m, tileB, lane);
+    } else {
+        __shared__ HeavyLds<kUnrollWide> sm;
+        down_heavy(lo, l, dt, active, bk, m, tileB, threadIdx.x, sm);
+    }
 }
 
 // ---------------------------------------------------------------- fp32
@@ -329,20 +505,31 @@ __global__ __launch_bounds__(64) void combine_kernel(Layout lo, int l, float* __
 }  // namespace
 
 hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st) {
-    if (lo.dtype == 1)
-        hipLaunchKernelGGL(ffn_up_bf16, dim3(lo.max_units * (lo.F / 16)), dim3(64), 0, st, lo, l, bbuf, sv,
-                           static_cast<const uint16_t*>(h));
-    else
+    if (lo.dtype == 1) {
+        const uint16_t* hb = static_cast<const uint16_t*>(h);
+        if (lo.ffn_waves == kWaves)
+            hipLaunchKernelGGL(ffn_up_bf16<kWaves>, dim3(lo.max_units * (lo.F / (16 * kWaves))), dim3(64 * kWaves), 0,
+                               st, lo, l, bbuf, sv, hb);
+        else
+            hipLaunchKernelGGL(ffn_up_bf16<1>, dim3(lo.max_units * (lo.F / 16)), dim3(64), 0, st, lo, l, bbuf, sv, hb);
+    } else {
         hipLaunchKernelGGL(ffn_up_f32, dim3(lo.N * (lo.F / 64)), dim3(64), 0, st, lo, l, bbuf, sv,
                            static_cast<const float*>(h));
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st) {
-    if (lo.dtype == 1)
-        hipLaunchKernelGGL(ffn_down_bf16, dim3(lo.max_units * (lo.d / 32)), dim3(64), 0, st, lo, l, bbuf, sv);
-    else
+    if (lo.dtype == 1) {
+        const int dtn = lo.d / 32;
+        if (lo.ffn_waves == kWaves)
+            hipLaunchKernelGGL(ffn_down_bf16<kWaves>, dim3(lo.max_units * ((dtn + kWaves - 1) / kWaves)),
+                               dim3(64 * kWaves), 0, st, lo, l, bbuf, sv);
+        else
+            hipLaunchKernelGGL(ffn_down_bf16<1>, dim3(lo.max_units * dtn), dim3(64), 0, st, lo, l, bbuf, sv);
+    } else {
         hipLaunchKernelGGL(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), 0, st, lo, l, bbuf, sv);
+    }
     return hipGetLastError();
 }
 

@@ -70,6 +70,7 @@ def test_query_arena_is_capped_by_n_slots():
     (dict(policy=3, lrfu_lambda=float("nan")), B.CMOE_ERR_INVALID_ARG),
     (dict(policy=3, lrfu_lambda=float("inf")), B.CMOE_ERR_INVALID_ARG),
     (dict(dtype=5), B.CMOE_ERR_INVALID_ARG),
+    (dict(flags=B.CMOE_FLAG_FFN_GROUPED | B.CMOE_FLAG_FFN_SINGLE), B.CMOE_ERR_INVALID_ARG),
     (dict(N=300, C=6), B.CMOE_ERR_UNSUPPORTED),
     (dict(d=200), B.CMOE_ERR_UNSUPPORTED),
     (dict(F=100), B.CMOE_ERR_UNSUPPORTED),
@@ -82,7 +83,8 @@ def test_query_rejects_invalid_configs(kw, status):
 
 
 @pytest.mark.parametrize("kw", [dict(policy=1), dict(policy=2), dict(policy=3, lrfu_lambda=0.0),
-                                dict(mode=2, policy=1, R=3), dict(mode=2, policy=3, R=16)])
+                                dict(mode=2, policy=1, R=3), dict(mode=2, policy=3, R=16),
+                                dict(flags=B.CMOE_FLAG_FFN_GROUPED), dict(flags=B.CMOE_FLAG_FFN_SINGLE)])
 def test_query_accepts_policy_configs(kw):
     st, out = query(**kw)
     assert st == B.CMOE_OK

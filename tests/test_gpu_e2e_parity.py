@@ -56,11 +56,11 @@ def test_device_generator_matches_host_twin():
         del inp
 
 
-def run_e2e(w, T, tol, check_ffn_every=1, samples=None):
+def run_e2e(w, T, tol, check_ffn_every=1, samples=None, ffn_shape=None):
     from paper_2609_04895_amd import cmoe as B
     from paper_2609_04895_amd.workload import engine_for
     inp = synth.device_inputs(w, T=T)
-    eng = engine_for(w, inp)
+    eng = engine_for(w, inp, ffn_shape=ffn_shape)
     dev = torch.device("cuda", 0)
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device=dev)
     # host copies of what the oracle needs
@@ -133,21 +133,26 @@ def test_bf16_full_mode_small_shape():
     run_e2e(w, T=10, tol=2e-2)
 
 
-def test_bf16_ragged_chunks_and_zipf_bias():
-    # d = 320 and F = 192 are not multiples of 256: exercises the chunk tails;
-    # many tokens per expert (N = 16, S = 40) exercises several token groups
+@pytest.mark.parametrize("shape", ["single", "grouped"])
+def test_bf16_ragged_chunks_and_zipf_bias(shape):
+    # d = 320 and F = 192 are not multiples of 256: exercises the chunk tails
+    # (an odd number of 64-wide chunks; grouped down workgroups whose last
+    # wavefronts have no d-tile); many tokens per expert (N = 16, S = 40)
+    # exercises several token groups
     w = synth.WORKLOADS["qwen3_30b_zipf"].replace(name="bf16_ragged", L=2, N=16, K=4, d=320, F=192, S=40, C=6,
                                                   R=2)
-    run_e2e(w, T=6, tol=2e-2)
+    run_e2e(w, T=6, tol=2e-2, ffn_shape=shape)
 
 
-def test_bf16_hot_experts_span_several_ffn_units():
+@pytest.mark.parametrize("shape", ["single", "grouped"])
+def test_bf16_hot_experts_span_several_ffn_units(shape):
     # 160 streams over 8 Zipf-biased experts: the hottest buckets hold well
     # over 64 tokens, so they are cut into several FFN work units, ranked by
-    # size; every output is checked
+    # size; every output is checked, with one-wavefront workgroups and with
+    # grouped ones (activations of big units shared through LDS)
     w = synth.WORKLOADS["qwen3_30b_zipf"].replace(name="bf16_hot_units", L=2, N=8, K=2, d=256, F=128, S=160, C=4,
                                                   R=2)
-    run_e2e(w, T=4, tol=2e-2)
+    run_e2e(w, T=4, tol=2e-2, ffn_shape=shape)
 
 
 def test_bf16_256_experts_full_mode():
