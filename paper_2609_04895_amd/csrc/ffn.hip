@@ -35,7 +35,10 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kNG = 4;          // token groups (of 16) per pass when a unit holds more than 16
 static_assert(kUnitTokens == 16 * kNG, "one work unit is one pass over the weights");
 constexpr int kUnroll = 4;      // k chunks per load block, one token group
-constexpr int kUnrollWide = 2;  // k chunks per load block, kNG token groups
+constexpr int kUnrollWide = 2;  // k chunks per load block, kNG token groups sharing LDS (grouped launch)
+constexpr int kUnrollSolo = 1;  // k chunks per load block, kNG token groups in one wavefront: this
+                                // path is rare in the launches that use it, and a deeper block would
+                                // set the register budget (and so the occupancy) of the whole kernel
 constexpr int kWaves = 4;       // wavefronts per grouped workgroup: consecutive row tiles of one work unit
 
 __device__ inline bf16x8 as_bf16x8(uint4 v) {
@@ -165,21 +168,28 @@ __device__ inline Staged stage_load(const uint16_t* const* xb, int c, int nchunk
     return st;
 }
 
+// LDS stores of the ng groups in use (wavefront-uniform).
 template <int U>
-__device__ inline void stage_store(uint4 (*xs)[64], int tid, const Staged& st) {
+__device__ inline void stage_store(uint4 (*xs)[64], int tid, int ng, const Staged& st) {
     const int i = tid >> 7, hh = (tid >> 6) & 1;
 #pragma unroll
-    for (int q = 0; q < kNG; ++q) xs[(q * U + i) * 2 + hh][tid & 63] = st.v[q];
+    for (int q = 0; q < kNG; ++q)
+        if (q < ng) xs[(q * U + i) * 2 + hh][tid & 63] = st.v[q];
 }
 
-// One pass of kNG token groups over a 16-row (gate/up) or 2 x 16-row (down)
-// weight tile with the activations shared through LDS.  Every wavefront of
-// the workgroup runs the loop (and its barriers); `active` wavefronts also
-// load their weights and run the matrix-core work.
+// One pass of ng (up to kNG) token groups over a 16-row (gate/up) or
+// 2 x 16-row (down) weight tile with the activations shared through LDS.
+// Every wavefront of the workgroup runs the loop (and its barriers); only
+// `active` wavefronts run the matrix-core work.  Every global load is
+// unconditional, so that the waits before the LDS stores cover the staging
+// loads only: the weight loads of an inactive wavefront re-read its tile's
+// first chunk (cached), and staging loads of unused groups repeat the last
+// token.
 template <int U>
-__device__ inline void mfma_pass_shared(const uint4* __restrict__ tile, int nchunk, const uint16_t* const* xb,
+__device__ inline void mfma_pass_shared(const uint4* __restrict__ tile, int nchunk, const uint16_t* const* xb, int ng,
                                         bool active, HeavyLds<U>& sm, int tid, f32x4* acc0, f32x4* acc1) {
     const int lane = tid & 63;
+    ng = __builtin_amdgcn_readfirstlane(ng);
 #pragma unroll
     for (int q = 0; q < kNG; ++q) {
         acc0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -192,22 +202,21 @@ __device__ inline void mfma_pass_shared(const uint4* __restrict__ tile, int nchu
     int b = 0;
     for (int c = 0; c < nchunk; c += U, b ^= 1) {
         uint4 A[U][4];
-        if (active) {
 #pragma unroll
-            for (int i = 0; i < U; ++i) {
-                const uint4* ch = tile + (int64_t)min(c + i, nchunk - 1) * 256;
-                A[i][0] = load_stream(ch);
-                A[i][1] = load_stream(ch + 64);
-                A[i][2] = load_stream(ch + 128);
-                A[i][3] = load_stream(ch + 192);
-            }
+        for (int i = 0; i < U; ++i) {
+            const uint4* ch = tile + (int64_t)(active ? min(c + i, nchunk - 1) : 0) * 256;
+            A[i][0] = load_stream(ch);
+            A[i][1] = load_stream(ch + 64);
+            A[i][2] = load_stream(ch + 128);
+            A[i][3] = load_stream(ch + 192);
         }
-        stage_store<U>(sm.x[b], tid, st);
+        stage_store<U>(sm.x[b], tid, ng, st);
         __syncthreads();
         st = stage_load<U>(xb, c + U, nchunk, tid);
         if (!active) continue;
 #pragma unroll
         for (int q = 0; q < kNG; ++q) {
+            if (q >= ng) break;
             uint4 X[U][2];
 #pragma unroll
             for (int i = 0; i < U; ++i) {
@@ -278,7 +287,7 @@ __device__ inline void up_heavy(const Layout& lo, int l, int ft, const int32_t* 
 #pragma unroll
     for (int q = 0; q < kNG; ++q) xb[q] = h + ((int64_t)(pr[q] >> 8) * lo.L + l) * d + 8 * g;
     f32x4 cg[kNG], cu[kNG];
-    mfma_pass_shared<kUnrollWide>(tileA, d / 64, xb, true, sm, tid, cg, cu);
+    mfma_pass_shared<kUnrollWide>(tileA, d / 64, xb, (m + 15) / 16, true, sm, tid, cg, cu);
 #pragma unroll
     for (int q = 0; q < kNG; ++q) {
         const int tok = 16 * q + r;
@@ -319,7 +328,7 @@ __global__ __launch_bounds__(64 * W) void ffn_up_bf16(Layout lo, int l, int bbuf
     if (m <= 16) {  // workgroup-uniform
         up_passes<1, kUnroll>(lo, l, ft, bk, m, tileA, h, lane);
     } else if constexpr (W == 1) {
-        up_passes<kNG, kUnrollWide>(lo, l, ft, bk, m, tileA, h, lane);
+        up_passes<kNG, kUnrollSolo>(lo, l, ft, bk, m, tileA, h, lane);
     } else {
         __shared__ HeavyLds<kUnrollWide> sm;
         up_heavy(lo, l, ft, bk, m, tileA, h, threadIdx.x, sm);
@@ -374,7 +383,7 @@ __device__ inline void down_heavy(const Layout& lo, int l, int dt, bool active, 
 #pragma unroll
     for (int q = 0; q < kNG; ++q) xb[q] = act + ((int64_t)(pr[q] >> 8) * lo.K + (pr[q] & 255)) * F + 8 * g;
     f32x4 c0[kNG], c1[kNG];
-    mfma_pass_shared<kUnrollWide>(tileB, F / 64, xb, active, sm, tid, c0, c1);
+    mfma_pass_shared<kUnrollWide>(tileB, F / 64, xb, (m + 15) / 16, active, sm, tid, c0, c1);
     if (!active) return;
 #pragma unroll
     for (int q = 0; q < kNG; ++q) {
@@ -414,7 +423,7 @@ __global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bb
     if (m <= 16) {  // workgroup-uniform; this path has no barriers
         if (active) down_passes<1, kUnroll>(lo, l, dt, bk, m, tileB, lane);
     } else if constexpr (W == 1) {
-        down_passes<kNG, kUnrollWide>(lo, l, dt, bk, m, tileB, lane);
+        down_passes<kNG, kUnrollSolo>(lo, l, dt, bk, m, tileB, lane);
     } else {
         __shared__ HeavyLds<kUnrollWide> sm;
         down_heavy(lo, l, dt, active, bk, m, tileB, threadIdx.x, sm);
