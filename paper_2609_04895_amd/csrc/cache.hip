@@ -340,6 +340,8 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
         }
         if (refine) ctr_rp = lo.ctr[((int64_t)s * L + a.rl) * kNctr + kCtrP];
     }
+    int64_t bucket = 0;  // lane k < K: bucket of its selection and position in it
+    int bucket_pos = 0;
     float polv[NPL];  // classical priority of the accessed layer
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
@@ -445,14 +447,12 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             lo.gates[o] = my_p / gsum;
             // token (s, k) joins the bucket of its expert; the position inside
             // the bucket does not affect any result (each token is its own
-            // column of the expert's matrix products)
-            const int64_t be = (int64_t)a.bbuf * N + my_sel;
-            const int pos = atomicAdd(&lo.bcount[be], 1);
-            lo.pairs[be * lo.S + pos] = (s << 8) | lane;
-            if (counted) {
-                if (pos == 0) atomicAdd(&lo.active_sum[l], 1ull);
-                atomicAdd(&lo.selcount[(int64_t)l * N + my_sel], 1ull);
-            }
+            // column of the expert's matrix products).  The position is used
+            // at the end of the step, so the atomic's round trip overlaps the
+            // rest of it.
+            bucket = (int64_t)a.bbuf * N + my_sel;
+            bucket_pos = atomicAdd(&lo.bcount[bucket], 1);
+            if (counted) atomicAdd(&lo.selcount[(int64_t)l * N + my_sel], 1ull);
         }
         // retention priority of Algorithm 1
         float sT[NPL];
@@ -545,6 +545,10 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
         }
     }
     if (refine) refine_one<NPL>(lo, s, a.rl, a.R, a.t, counted, pred, aTv, cw_r, ctr_rp, lane);
+    if ((a.flags & kFlagAccess) && lane < K) {
+        lo.pairs[bucket * lo.S + bucket_pos] = (s << 8) | lane;
+        if (counted && bucket_pos == 0) atomicAdd(&lo.active_sum[a.l], 1ull);
+    }
 }
 
 template <int NPL, int NR, bool INJECT, int ZS>
