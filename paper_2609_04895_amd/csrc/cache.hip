@@ -135,68 +135,108 @@ __device__ inline int argmax_lowest(const uint32_t (&key)[NPL], uint32_t& kmax) 
     return e;
 }
 
-__device__ inline float wave_max_f32(float v) {
-    unsigned u = __float_as_uint(v);
-    u = __float_as_uint(fmaxf(__uint_as_float(u), __uint_as_float(dpp<kQuadXor1>(u))));
-    u = __float_as_uint(fmaxf(__uint_as_float(u), __uint_as_float(dpp<kQuadXor2>(u))));
-    u = __float_as_uint(fmaxf(__uint_as_float(u), __uint_as_float(dpp<kRowHalfMirror>(u))));
-    u = __float_as_uint(fmaxf(__uint_as_float(u), __uint_as_float(dpp<kRowMirror>(u))));
-    const auto p = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-    u = __float_as_uint(fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1])));
-    const auto q = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-    u = __float_as_uint(fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1])));
-    return __uint_as_float(__builtin_amdgcn_readfirstlane(u));
-}
-
-// Strided-halving sum of lanes [0, P) for a power of two P <= 64: at
-// w = P/2 .. 1, lane i < w adds lane i + w (the tree of lane 0 is exactly
-// that order); returns lane 0's total to every lane.
-__device__ inline float wave_sum_halving(float x, int P) {
-    if (P >= 64) {
-        const unsigned u = __float_as_uint(x);
-        const auto q = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-        x = x + __uint_as_float(q[1]);  // lanes < 32: lane + 32
-    }
-    if (P >= 32) {
-        const unsigned u = __float_as_uint(x);
-        const auto q = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-        x = x + __uint_as_float(q[1]);  // lanes of even rows: lane + 16
-    }
-    if (P >= 16) x = x + __uint_as_float(dpp<kRowShl1 + 7>(__float_as_uint(x)));
-    if (P >= 8) x = x + __uint_as_float(dpp<kRowShl1 + 3>(__float_as_uint(x)));
-    if (P >= 4) x = x + __uint_as_float(dpp<kRowShl1 + 1>(__float_as_uint(x)));
-    if (P >= 2) x = x + __uint_as_float(dpp<kRowShl1>(__float_as_uint(x)));
-    return __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 0));
-}
-
-template <int NPL>
-__device__ inline void softmax_fixed(const float (&z)[NPL], int N, int lane, float (&p)[NPL]) {
-    float m = -INFINITY;
+// The fixed softmax (described at the top of this file) of R independent
+// logit vectors, step by step for all of them at once so that the latencies
+// of their cross-lane reductions overlap.  Wavefront maximum: DPP and
+// permlane-swap max steps; sum: strided halving over the next power of two
+// P >= N, in-lane adds for w >= 64, then for w = 32 .. 1 lane i < w adds lane
+// i + w (the tree of lane 0 is exactly that order), lane 0's total taken.
+template <int NPL, int R>
+__device__ inline void softmax_fixed(const float (&z)[3][NPL], int N, int lane, float (&p)[3][NPL]) {
+    unsigned u[R];
 #pragma unroll
-    for (int j = 0; j < NPL; ++j)
-        if (j * 64 + lane < N) m = fmaxf(m, z[j]);
-    m = wave_max_f32(m);
-    float v[NPL];
+    for (int r = 0; r < R; ++r) {
+        float m = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < NPL; ++j) {
-        const bool in = j * 64 + lane < N;
-        p[j] = in ? canon_exp(z[j] - m) : 0.0f;
-        v[j] = p[j];
+        for (int j = 0; j < NPL; ++j)
+            if (j * 64 + lane < N) m = fmaxf(m, z[r][j]);
+        u[r] = __float_as_uint(m);
+    }
+    // wavefront maxima
+#pragma unroll
+    for (int r = 0; r < R; ++r) u[r] = __float_as_uint(fmaxf(__uint_as_float(u[r]), __uint_as_float(dpp<kQuadXor1>(u[r]))));
+#pragma unroll
+    for (int r = 0; r < R; ++r) u[r] = __float_as_uint(fmaxf(__uint_as_float(u[r]), __uint_as_float(dpp<kQuadXor2>(u[r]))));
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        u[r] = __float_as_uint(fmaxf(__uint_as_float(u[r]), __uint_as_float(dpp<kRowHalfMirror>(u[r]))));
+#pragma unroll
+    for (int r = 0; r < R; ++r) u[r] = __float_as_uint(fmaxf(__uint_as_float(u[r]), __uint_as_float(dpp<kRowMirror>(u[r]))));
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const auto q = __builtin_amdgcn_permlane16_swap(u[r], u[r], false, false);
+        u[r] = __float_as_uint(fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1])));
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const auto q = __builtin_amdgcn_permlane32_swap(u[r], u[r], false, false);
+        u[r] = __float_as_uint(fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1])));
+    }
+    float v[R][NPL];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float m = __uint_as_float(__builtin_amdgcn_readfirstlane(u[r]));
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+            const bool in = j * 64 + lane < N;
+            p[r][j] = in ? canon_exp(z[r][j] - m) : 0.0f;
+            v[r][j] = p[r][j];
+        }
     }
     int P = 1;
     while (P < N) P <<= 1;
-    // in-lane halving steps (w >= 64)
 #pragma unroll
     for (int jw = NPL / 2; jw >= 1; jw >>= 1) {
         if (jw * 64 * 2 <= P) {
 #pragma unroll
-            for (int j = 0; j < jw; ++j) v[j] = v[j] + v[j + jw];
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int j = 0; j < jw; ++j) v[r][j] = v[r][j] + v[r][j + jw];
         }
     }
     // cross-lane halving steps (w < 64)
-    const float sum = wave_sum_halving(v[0], P < 64 ? P : 64);
+    const int Pw = P < 64 ? P : 64;
+    float x[R];
 #pragma unroll
-    for (int j = 0; j < NPL; ++j) p[j] = p[j] / sum;
+    for (int r = 0; r < R; ++r) x[r] = v[r][0];
+    if (Pw >= 64) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const unsigned w = __float_as_uint(x[r]);
+            const auto q = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+            x[r] = x[r] + __uint_as_float(q[1]);
+        }
+    }
+    if (Pw >= 32) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const unsigned w = __float_as_uint(x[r]);
+            const auto q = __builtin_amdgcn_permlane16_swap(w, w, false, false);
+            x[r] = x[r] + __uint_as_float(q[1]);
+        }
+    }
+    if (Pw >= 16) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) x[r] = x[r] + __uint_as_float(dpp<kRowShl1 + 7>(__float_as_uint(x[r])));
+    }
+    if (Pw >= 8) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) x[r] = x[r] + __uint_as_float(dpp<kRowShl1 + 3>(__float_as_uint(x[r])));
+    }
+    if (Pw >= 4) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) x[r] = x[r] + __uint_as_float(dpp<kRowShl1 + 1>(__float_as_uint(x[r])));
+    }
+    if (Pw >= 2) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) x[r] = x[r] + __uint_as_float(dpp<kRowShl1>(__float_as_uint(x[r])));
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float sum = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x[r]), 0));
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) p[r][j] = p[r][j] / sum;
+    }
 }
 
 template <int NPL>
@@ -404,11 +444,17 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
                 z[r][j] = e < N ? v : 0.0f;
             }
         }
-        // router slots: 0 native, then temporal (router policy), then spatio
+        // router slots: 0 native, then temporal (router policy), then spatio;
+        // every slot is in use, so the NR softmaxes run together
+        float pz[3][NPL];
+        softmax_fixed<NPL, NR>(z, N, lane, pz);
         float pR[NPL], pT[NPL];
-        softmax_fixed<NPL>(z[0], N, lane, pR);
-        if (NR >= 2 && !classical) softmax_fixed<NPL>(z[1], N, lane, pT);
-        if (NR >= 2 && spatio) softmax_fixed<NPL>(z[NR - 1], N, lane, pred);
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+            pR[j] = pz[0][j];
+            pT[j] = (NR >= 2 && !classical) ? pz[1][j] : 0.0f;
+            if (NR >= 2 && spatio) pred[j] = pz[NR - 1][j];
+        }
 
         // Top-K by native logit, lower index first on ties
         uint32_t key[NPL];  // ordered native logits; 0 = taken or past N (no real logit maps to 0)
