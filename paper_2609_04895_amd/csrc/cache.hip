@@ -92,9 +92,12 @@ __device__ inline uint32_t ord32(float x) {
 // the pair {own value, value of lane ^ 16} in some order (permlane32_swap:
 // lane ^ 32), so an order-free combine of the pair is the combine with that
 // partner.
+// Lanes whose source is outside their row read 0 (bound_ctrl); no step
+// below uses such a lane's result.  The move folds into the consuming
+// max or add as one DPP instruction.
 template <int CTRL>
 __device__ inline unsigned dpp(unsigned v) {
-    return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xF, 0xF, false);
+    return (unsigned)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
 }
 constexpr int kQuadXor1 = 0xB1;     // quad_perm 1,0,3,2
 constexpr int kQuadXor2 = 0x4E;     // quad_perm 2,3,0,1
