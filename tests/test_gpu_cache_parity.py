@@ -52,6 +52,7 @@ CASES = [
     (2, 64, 64, 64, 64, 2, 1, 0, True, False),   # K = C = N = R
     (2, 1, 1, 1, 1, 2, 1, 0, False, True),       # a single expert
     (2, 256, 8, 16, 4, 300, 1, 0, True, True),   # 1200 cache words per layer: several per fill thread
+    (1, 32, 4, 8, 3, 5, 1, 0, True, True),       # one layer: its causal predecessor is itself, one token back
 ]
 
 

@@ -174,6 +174,15 @@ def test_bf16_update_only_gptoss_like():
     run_e2e(w, T=8, tol=2e-2)
 
 
+@pytest.mark.parametrize("dtype", [synth.DTYPE_BF16, synth.DTYPE_F32])
+def test_single_layer_smallest_dims(dtype):
+    # L = 1 (the refinement of each token reads the same layer's previous
+    # prediction), d = F = 64 (one k chunk: every load block is a tail)
+    w = synth.WORKLOADS["qwen3_30b"].replace(name=f"min_dims_{dtype}", L=1, N=8, K=2, d=64, F=64, S=5, C=3, R=2,
+                                             mode=synth.MODE_SPATIO_TEMPORAL, dtype=dtype)
+    run_e2e(w, T=8, tol=2e-2 if dtype == synth.DTYPE_BF16 else 1e-5)
+
+
 def test_bf16_top11_output_combine():
     # K = 11: the output combine adds a full batch of eight gated outputs and
     # a clamped batch of three, in k order

@@ -53,6 +53,7 @@ CASES = [
     (2, 256, 8, 40, 12, 6, SPATIO_ONLY, LFU, 0.5, 0, True, True),   # four experts per lane
     (2, 64, 64, 64, 64, 2, SPATIO_ONLY, LRU, 0.5, 0, True, False),  # K = C = N = R
     (2, 1, 1, 1, 1, 2, SPATIO_ONLY, LRFU, 0.5, 0, False, True),     # a single expert
+    (1, 16, 2, 4, 2, 3, SPATIO_ONLY, LRU, 0.5, 0, True, True),      # a single layer
 ]
 
 
