@@ -153,7 +153,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.act = take(S * K * (size_t)c->F * dv.esz);
     p.yp = take(S * K * (size_t)c->d * 4);
     p.zero_row = take(N * 4);
-    p.units = take((size_t)max_units(c) * 4);
+    p.units = take((size_t)max_units(c) * 16);
     p.ws_total = o;
     p.arena = L * (size_t)dv.n_slots * dv.expert_bytes;
     return p;

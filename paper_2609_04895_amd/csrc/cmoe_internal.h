@@ -57,8 +57,9 @@ struct Layout {
     void* act;                  // [S][K][F]   SwiGLU intermediate (dtype)
     float* yp;                  // [S][K][d]   gated expert outputs
     float* zero_row;            // [N]         zeros (native bias when there is none)
-    int32_t* units;             // [max_units] FFN work units of the layer step, heaviest
-                                //             first: (pass << 8) | expert, -1 past the end
+    int32_t* units;             // [max_units][4] FFN work units of the layer step, heaviest
+                                //             first: {(pass << 8) | expert, slot, tokens, 0},
+                                //             {-1, -1, 0, 0} past the end
 };
 
 // cache-step kernel flags

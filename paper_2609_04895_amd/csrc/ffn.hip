@@ -70,14 +70,6 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
     return (a >> 16) | (b & 0xFFFF0000u);
 }
 
-// Slot of expert e of layer l (slot map version sv), or -1 if it has none
-// (cannot happen for a selected expert: the residency step maps every member
-// of any cache, and selected experts are members).
-__device__ inline int expert_slot(const Layout& lo, int l, int sv, int e) {
-    const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
-    return (slot < 0 || slot >= lo.n_slots) ? -1 : slot;
-}
-
 __device__ inline const uint16_t* slot_base(const Layout& lo, int l, int slot) {
     return reinterpret_cast<const uint16_t*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems;
 }
@@ -314,12 +306,10 @@ __global__ __launch_bounds__(64 * W) void ffn_up_bf16(Layout lo, int l, int bbuf
     const int u = blockIdx.x / wgn;
     const int lane = threadIdx.x & 63;
     const int ft = (blockIdx.x - u * wgn) * W + (threadIdx.x >> 6);
-    const int unit = lo.units[u];
-    if (unit < 0) return;
-    const int e = unit & 255, t0 = kUnitTokens * (unit >> 8);
-    const int slot = expert_slot(lo, l, sv, e);
-    const int m = min(kUnitTokens, lo.bcount[(int64_t)bbuf * lo.N + e] - t0);
-    if (m <= 0 || slot < 0) return;
+    const int4 ui = reinterpret_cast<const int4*>(lo.units)[u];  // expert, pass, slot, tokens in one load
+    if (ui.x < 0) return;
+    const int e = ui.x & 255, t0 = kUnitTokens * (ui.x >> 8), slot = ui.y, m = ui.z;
+    if (m <= 0 || slot < 0 || slot >= lo.n_slots) return;
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S + t0;
     // packed slot layout: chunk c of this row tile is 256 units of 16 bytes,
     // gate half 0, gate half 1, up half 0, up half 1, each 64 units
@@ -408,12 +398,10 @@ __global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bb
     const int lane = threadIdx.x & 63;
     const int dt = (blockIdx.x - u * wgn) * W + (threadIdx.x >> 6);
     const bool active = dt < dtn;
-    const int unit = lo.units[u];
-    if (unit < 0) return;
-    const int e = unit & 255, t0 = kUnitTokens * (unit >> 8);
-    const int slot = expert_slot(lo, l, sv, e);
-    const int m = min(kUnitTokens, lo.bcount[(int64_t)bbuf * lo.N + e] - t0);
-    if (m <= 0 || slot < 0) return;
+    const int4 ui = reinterpret_cast<const int4*>(lo.units)[u];  // expert, pass, slot, tokens in one load
+    if (ui.x < 0) return;
+    const int e = ui.x & 255, t0 = kUnitTokens * (ui.x >> 8), slot = ui.y, m = ui.z;
+    if (m <= 0 || slot < 0 || slot >= lo.n_slots) return;
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S + t0;
     // packed slot layout: after the gate/up part (F d / 4 units), chunk c of
     // this 32-row tile is 256 units: rows 0-15 half 0, half 1, rows 16-31

@@ -173,18 +173,22 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
         }
     }
     // FFN work units of this layer step: each expert's bucket cut into passes
-    // of up to kUnitTokens tokens.  When no bucket needs a second pass, unit e
-    // is expert e (or -1 if it has no tokens).
+    // of up to kUnitTokens tokens, each stored with its expert's new slot and
+    // its token count, so that an FFN wavefront finds all three with one load.
+    // When no bucket needs a second pass, unit e is expert e (or none if it
+    // has no tokens).
+    int4* unit4 = reinterpret_cast<int4*>(lo.units);
     const bool multi = __syncthreads_or(units && m_own > kUnitTokens) != 0;
     if (units && !multi) {
         // blockDim.x >= N: thread e holds expert e's bucket size
-        for (int i = tid; i < lo.max_units; i += blockDim.x) lo.units[i] = (i < N && m_own > 0) ? i : -1;
+        for (int i = tid; i < lo.max_units; i += blockDim.x)
+            unit4[i] = (i < N && m_own > 0) ? int4{i, so[i], m_own, 0} : int4{-1, -1, 0, 0};
     } else if (units) {
         // otherwise experts with more tokens go first (lower index on ties),
         // so the longest units start first.  Rank of expert e = number of
         // larger keys (m << 8) | (255 - e), all distinct.
         __shared__ __align__(16) int key[kMaxN];
-        __shared__ int by_rank[kMaxN], who[kMaxN];
+        __shared__ int by_rank[kMaxN], who[kMaxN], m_rank[kMaxN];
         const int m = m_own;
         const int mykey = (m << 8) | (255 - tid);
         key[tid] = tid < N ? mykey : -1;  // blockDim.x == kMaxN: every entry is written
@@ -200,14 +204,18 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
         if (tid < N) {
             by_rank[rank] = (m + kUnitTokens - 1) / kUnitTokens;
             who[rank] = tid;
+            m_rank[rank] = m;
         }
         __syncthreads();
         const int passes = tid < N ? by_rank[tid] : 0;
         int total;
         const int off = block_scan(passes, &total, lds4);
-        if (tid < N)
-            for (int q = 0; q < passes; ++q) lo.units[off + q] = (q << 8) | who[tid];
-        for (int i = total + tid; i < lo.max_units; i += blockDim.x) lo.units[i] = -1;
+        if (tid < N) {
+            const int e = who[tid];
+            for (int q = 0; q < passes; ++q)
+                unit4[off + q] = int4{(q << 8) | e, so[e], min(kUnitTokens, m_rank[tid] - kUnitTokens * q), 0};
+        }
+        for (int i = total + tid; i < lo.max_units; i += blockDim.x) unit4[i] = int4{-1, -1, 0, 0};
     }
     if (nenter == 0) return;
     const int64_t bytes = lo.expert_elems * (lo.dtype == 1 ? 2 : 4);
