@@ -251,16 +251,17 @@ size_t cmoe_view_bytes(const cmoe_handle* hd, int32_t view);
 /* Copies a view into host memory of at least cmoe_view_bytes bytes. */
 cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t bytes);
 
-/* Per-kernel timing with HIP events recorded on the stream each kernel runs
- * on.  cmoe_profile_begin makes the next max_tokens calls of cmoe_step /
- * cmoe_step_logits record a start/stop event pair around each launch of the
- * kernels selected by kernel_mask (bit i = kernel id i; 0 selects all);
+/* Per-kernel timing with HIP events.  cmoe_profile_begin makes the next
+ * max_tokens calls of cmoe_step / cmoe_step_logits attach a start/stop event
+ * pair to each launch of the kernels selected by kernel_mask (bit i = kernel
+ * id i; 0 selects all): the events take the kernel's own start and end
+ * timestamps (hipExtLaunchKernel);
  * cmoe_profile_end synchronizes and returns, per kernel id, the summed
  * milliseconds and the launch count.  Kernel ids: 0 router GEMV, 1 cache
  * step (routing, refinement, retention, counters, expert grouping),
  * 2 residency and fill, 3 expert gate/up, 4 expert down, 5 combine.
- * ms_out and launches_out hold CMOE_KERNEL_COUNT entries.  Event pairs add
- * work between launches; time few kernels at once. */
+ * ms_out and launches_out hold CMOE_KERNEL_COUNT entries.  Timed launches
+ * carry extra bookkeeping; time few kernels at once. */
 #define CMOE_KERNEL_COUNT 6
 cmoe_status cmoe_profile_begin(cmoe_handle* hd, int32_t max_tokens, uint32_t kernel_mask);
 cmoe_status cmoe_profile_end(cmoe_handle* hd, double* ms_out, int64_t* launches_out);

@@ -646,29 +646,29 @@ hipError_t launch_init(const Layout& lo, hipStream_t st) {
 }
 
 template <int NPL, int NR>
-hipError_t launch_step_nr(const Layout& lo, const StepArgs& a, hipStream_t st) {
+hipError_t launch_step_nr(const Layout& lo, const StepArgs& a, hipStream_t st, const Timing& tm) {
     const dim3 grid((lo.S + kStreamsPerBlock - 1) / kStreamsPerBlock);
     const dim3 block(64 * kStreamsPerBlock);
     if (a.flags & kFlagInject)
-        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, true, 2>), grid, block, 0, st, lo, a);
+        launch_kernel(cache_step_kernel<NPL, NR, true, 2>, grid, block, st, tm, lo, a);
     else if (lo.zstride == 4)
-        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, false, 4>), grid, block, 0, st, lo, a);
+        launch_kernel(cache_step_kernel<NPL, NR, false, 4>, grid, block, st, tm, lo, a);
     else
-        hipLaunchKernelGGL((cache_step_kernel<NPL, NR, false, kMaxSplit>), grid, block, 0, st, lo, a);
+        launch_kernel(cache_step_kernel<NPL, NR, false, kMaxSplit>, grid, block, st, tm, lo, a);
     return hipGetLastError();
 }
 
 template <int NPL>
-hipError_t launch_step_npl(const Layout& lo, const StepArgs& a, hipStream_t st) {
-    if (lo.n_r == 3) return launch_step_nr<NPL, 3>(lo, a, st);
-    if (lo.n_r == 2) return launch_step_nr<NPL, 2>(lo, a, st);
-    return launch_step_nr<NPL, 1>(lo, a, st);
+hipError_t launch_step_npl(const Layout& lo, const StepArgs& a, hipStream_t st, const Timing& tm) {
+    if (lo.n_r == 3) return launch_step_nr<NPL, 3>(lo, a, st, tm);
+    if (lo.n_r == 2) return launch_step_nr<NPL, 2>(lo, a, st, tm);
+    return launch_step_nr<NPL, 1>(lo, a, st, tm);
 }
 
-hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st) {
-    if (lo.N <= 64) return launch_step_npl<1>(lo, a, st);
-    if (lo.N <= 128) return launch_step_npl<2>(lo, a, st);
-    return launch_step_npl<4>(lo, a, st);
+hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st, const Timing& tm) {
+    if (lo.N <= 64) return launch_step_npl<1>(lo, a, st, tm);
+    if (lo.N <= 128) return launch_step_npl<2>(lo, a, st, tm);
+    return launch_step_npl<4>(lo, a, st, tm);
 }
 
 }  // namespace cmoe

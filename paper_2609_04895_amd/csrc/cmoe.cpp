@@ -201,28 +201,19 @@ cmoe_status usable(cmoe_handle* hd) {
     return CMOE_OK;
 }
 
-// Records the start event of a timed launch (when profiling) and returns its
-// slot, or SIZE_MAX.
-size_t prof_start(cmoe_handle* hd, int kid, hipStream_t st) {
-    if (hd->prof_left <= 0 || !((hd->prof_mask >> kid) & 1u) || hd->prof_next + 2 > hd->prof_pool.size())
-        return SIZE_MAX;
-    const size_t i = hd->prof_next;
-    hd->prof_next += 2;
-    (void)hipEventRecord(hd->prof_pool[i], st);
-    hd->prof_rec.emplace_back(kid, i);
-    return i;
-}
-
-void prof_stop(cmoe_handle* hd, size_t i, hipStream_t st) {
-    if (i != SIZE_MAX) (void)hipEventRecord(hd->prof_pool[i + 1], st);
-}
-
+// Runs launch(timing): when this kernel is being profiled, timing holds the
+// next start/stop event pair, which the launch attaches to the kernel itself.
 template <typename F>
-hipError_t timed(cmoe_handle* hd, int kid, hipStream_t st, F&& launch) {
-    const size_t i = prof_start(hd, kid, st);
-    const hipError_t e = launch();
-    prof_stop(hd, i, st);
-    return e;
+hipError_t timed(cmoe_handle* hd, int kid, F&& launch) {
+    cmoe::Timing tm;
+    if (hd->prof_left > 0 && ((hd->prof_mask >> kid) & 1u) && hd->prof_next + 2 <= hd->prof_pool.size()) {
+        const size_t i = hd->prof_next;
+        hd->prof_next += 2;
+        hd->prof_rec.emplace_back(kid, i);
+        tm.start = hd->prof_pool[i];
+        tm.stop = hd->prof_pool[i + 1];
+    }
+    return launch(tm);
 }
 
 // One residency event of `layer` on stream st; advances the layer's slot-map
@@ -230,7 +221,7 @@ hipError_t timed(cmoe_handle* hd, int kid, hipStream_t st, F&& launch) {
 hipError_t fill(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, hipStream_t st, int bbuf = -1) {
     FillArgs f{layer, kind, hd->ver[layer], counted ? 1 : 0, zero_pre ? 1 : 0, bbuf};
     hd->ver[layer] ^= 1;
-    return timed(hd, KID_FILL, st, [&] { return cmoe::launch_fill(hd->lo, f, st); });
+    return timed(hd, KID_FILL, [&](const cmoe::Timing& tm) { return cmoe::launch_fill(hd->lo, f, st, tm); });
 }
 
 // One decode token.  h == nullptr selects injected logits (no router, no FFN).
@@ -245,7 +236,8 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
 
     if (refine_on) {  // layer 0: refined from the previous token's last-layer prediction
         StepArgs a{0, 0, hd->R, 0, cmoe::kFlagRefine | count, hd->t, {nullptr, nullptr, nullptr}};
-        HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "refine layer 0");
+        HIPCHK(timed(hd, KID_CACHE, [&](const cmoe::Timing& tm) { return cmoe::launch_cache_step(lo, a, M, tm); }),
+               "refine layer 0");
         if (!hd->side_is_main) {
             HIPCHK(hipEventRecord(hd->ev_access[0], M), "event record");
             HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[0], 0), "stream wait");
@@ -254,7 +246,9 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
         if (!hd->side_is_main) HIPCHK(hipEventRecord(hd->ev_pro[0], Sd), "event record");
     }
     for (int l = 0; l < c.L; ++l) {
-        if (!inject) HIPCHK(timed(hd, KID_ROUTER, M, [&] { return cmoe::launch_router(lo, l, h, M); }), "router");
+        if (!inject)
+            HIPCHK(timed(hd, KID_ROUTER, [&](const cmoe::Timing& tm) { return cmoe::launch_router(lo, l, h, M, tm); }),
+                   "router");
         // the proactive fill of this layer reads its refined caches: it must end
         // before the access below changes them
         if (refine_on && !hd->side_is_main) HIPCHK(hipStreamWaitEvent(M, hd->ev_pro[l], 0), "stream wait");
@@ -267,7 +261,8 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
         StepArgs a{l, l + 1, hd->R, bbuf, flags, hd->t, {zR, nullptr, nullptr}};
         if (hd->dv.iT > 0) a.z[hd->dv.iT] = zT;
         if (hd->dv.iS > 0) a.z[hd->dv.iS] = zS;
-        HIPCHK(timed(hd, KID_CACHE, M, [&] { return cmoe::launch_cache_step(lo, a, M); }), "cache step");
+        HIPCHK(timed(hd, KID_CACHE, [&](const cmoe::Timing& tm) { return cmoe::launch_cache_step(lo, a, M, tm); }),
+               "cache step");
         hd->g += 1;
         // demand loads gate this layer's FFN; the same launch lays out the FFN work units
         HIPCHK(fill(hd, l, 0, counted, !refine_on, M, inject ? -1 : bbuf), "fill");
@@ -283,9 +278,14 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
         }
         if (!inject) {
             const int sv = hd->ver[l];
-            HIPCHK(timed(hd, KID_UP, M, [&] { return cmoe::launch_ffn_up(lo, l, bbuf, sv, h, M); }), "ffn up");
-            HIPCHK(timed(hd, KID_DOWN, M, [&] { return cmoe::launch_ffn_down(lo, l, bbuf, sv, M); }), "ffn down");
-            HIPCHK(timed(hd, KID_COMBINE, M, [&] { return cmoe::launch_combine(lo, l, y, M); }), "combine");
+            HIPCHK(timed(hd, KID_UP,
+                         [&](const cmoe::Timing& tm) { return cmoe::launch_ffn_up(lo, l, bbuf, sv, h, M, tm); }),
+                   "ffn up");
+            HIPCHK(timed(hd, KID_DOWN,
+                         [&](const cmoe::Timing& tm) { return cmoe::launch_ffn_down(lo, l, bbuf, sv, M, tm); }),
+                   "ffn down");
+            HIPCHK(timed(hd, KID_COMBINE, [&](const cmoe::Timing& tm) { return cmoe::launch_combine(lo, l, y, M, tm); }),
+                   "combine");
         }
     }
     hd->t += 1;

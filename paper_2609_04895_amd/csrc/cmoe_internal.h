@@ -2,6 +2,7 @@
 // translation units of libcmoe.so.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -90,12 +91,29 @@ struct FillArgs {
     int32_t bbuf;        // kind 0: bucket buffer of the layer step (builds the FFN work units)
 };
 
+// Optional timing of one launch: with events, they take the kernel's own
+// start and end timestamps (hipExtLaunchKernel), not those of markers
+// recorded on the stream around the launch.
+struct Timing {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+
+template <typename... KArgs, typename... Args>
+inline void launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t st, const Timing& tm,
+                          Args... args) {
+    if (tm.start)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, st, tm.start, tm.stop, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+}
+
 hipError_t launch_init(const Layout& lo, hipStream_t st);
-hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st);
-hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st);
-hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st);
-hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st);
-hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st);
-hipError_t launch_combine(const Layout& lo, int l, float* y, hipStream_t st);
+hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st, const Timing& tm = {});
+hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st, const Timing& tm = {});
+hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st, const Timing& tm = {});
+hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st,
+                         const Timing& tm = {});
+hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st, const Timing& tm = {});
+hipError_t launch_combine(const Layout& lo, int l, float* y, hipStream_t st, const Timing& tm = {});
 
 }  // namespace cmoe

@@ -501,38 +501,38 @@ __global__ __launch_bounds__(64) void combine_kernel(Layout lo, int l, float* __
 
 }  // namespace
 
-hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st) {
+hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st, const Timing& tm) {
     if (lo.dtype == 1) {
         const uint16_t* hb = static_cast<const uint16_t*>(h);
         if (lo.ffn_waves == kWaves)
-            hipLaunchKernelGGL(ffn_up_bf16<kWaves>, dim3(lo.max_units * (lo.F / (16 * kWaves))), dim3(64 * kWaves), 0,
-                               st, lo, l, bbuf, sv, hb);
+            launch_kernel(ffn_up_bf16<kWaves>, dim3(lo.max_units * (lo.F / (16 * kWaves))), dim3(64 * kWaves), st, tm,
+                          lo, l, bbuf, sv, hb);
         else
-            hipLaunchKernelGGL(ffn_up_bf16<1>, dim3(lo.max_units * (lo.F / 16)), dim3(64), 0, st, lo, l, bbuf, sv, hb);
+            launch_kernel(ffn_up_bf16<1>, dim3(lo.max_units * (lo.F / 16)), dim3(64), st, tm, lo, l, bbuf, sv, hb);
     } else {
-        hipLaunchKernelGGL(ffn_up_f32, dim3(lo.N * (lo.F / 64)), dim3(64), 0, st, lo, l, bbuf, sv,
-                           static_cast<const float*>(h));
+        launch_kernel(ffn_up_f32, dim3(lo.N * (lo.F / 64)), dim3(64), st, tm, lo, l, bbuf, sv,
+                      static_cast<const float*>(h));
     }
     return hipGetLastError();
 }
 
-hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st) {
+hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st, const Timing& tm) {
     if (lo.dtype == 1) {
         const int dtn = lo.d / 32;
         if (lo.ffn_waves == kWaves)
-            hipLaunchKernelGGL(ffn_down_bf16<kWaves>, dim3(lo.max_units * ((dtn + kWaves - 1) / kWaves)),
-                               dim3(64 * kWaves), 0, st, lo, l, bbuf, sv);
+            launch_kernel(ffn_down_bf16<kWaves>, dim3(lo.max_units * ((dtn + kWaves - 1) / kWaves)), dim3(64 * kWaves),
+                          st, tm, lo, l, bbuf, sv);
         else
-            hipLaunchKernelGGL(ffn_down_bf16<1>, dim3(lo.max_units * dtn), dim3(64), 0, st, lo, l, bbuf, sv);
+            launch_kernel(ffn_down_bf16<1>, dim3(lo.max_units * dtn), dim3(64), st, tm, lo, l, bbuf, sv);
     } else {
-        hipLaunchKernelGGL(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), 0, st, lo, l, bbuf, sv);
+        launch_kernel(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), st, tm, lo, l, bbuf, sv);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_combine(const Layout& lo, int l, float* y, hipStream_t st) {
+hipError_t launch_combine(const Layout& lo, int l, float* y, hipStream_t st, const Timing& tm) {
     const int64_t n = (int64_t)lo.S * (lo.d / 4);
-    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64), 0, st, lo, l, y);
+    launch_kernel(combine_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64), st, tm, lo, l, y);
     return hipGetLastError();
 }
 

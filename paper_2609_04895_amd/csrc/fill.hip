@@ -241,8 +241,8 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
 
 }  // namespace
 
-hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st) {
-    hipLaunchKernelGGL(fill_kernel, dim3(kFillBlocks), dim3(256), 0, st, lo, f);
+hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st, const Timing& tm) {
+    launch_kernel(fill_kernel, dim3(kFillBlocks), dim3(256), st, tm, lo, f);
     return hipGetLastError();
 }
 

@@ -155,24 +155,24 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_kernel(Layout lo, in
 }
 
 template <bool BF16>
-static void launch_router_t(const Layout& lo, int l, const void* h, hipStream_t st) {
+static void launch_router_t(const Layout& lo, int l, const void* h, hipStream_t st, const Timing& tm) {
     const int dk = lo.rdk;  // multiple of 32; the last split may be shorter (d % 32 == 0)
     const dim3 grid(lo.n_r * ((lo.N + 15) / 16) * ((lo.S + 15) / 16), 1, lo.nsplit);
     const dim3 block(64 * kRouterWaves);
     const int cpw = dk / 32;  // k chunks per wavefront
     if (cpw >= 4)
-        hipLaunchKernelGGL((router_kernel<BF16, 4>), grid, block, 0, st, lo, l, h, dk);
+        launch_kernel(router_kernel<BF16, 4>, grid, block, st, tm, lo, l, h, dk);
     else if (cpw >= 2)
-        hipLaunchKernelGGL((router_kernel<BF16, 2>), grid, block, 0, st, lo, l, h, dk);
+        launch_kernel(router_kernel<BF16, 2>, grid, block, st, tm, lo, l, h, dk);
     else
-        hipLaunchKernelGGL((router_kernel<BF16, 1>), grid, block, 0, st, lo, l, h, dk);
+        launch_kernel(router_kernel<BF16, 1>, grid, block, st, tm, lo, l, h, dk);
 }
 
-hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st) {
+hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st, const Timing& tm) {
     if (lo.dtype == 1)
-        launch_router_t<true>(lo, l, h, st);
+        launch_router_t<true>(lo, l, h, st, tm);
     else
-        launch_router_t<false>(lo, l, h, st);
+        launch_router_t<false>(lo, l, h, st, tm);
     return hipGetLastError();
 }
 
