@@ -133,15 +133,15 @@ def test_full_size_qwen3_30b_zipf_sweep_points(C, R):
     run_full(synth.WORKLOADS["qwen3_30b_zipf"].replace(C=C, R=R), T=10, ffn_samples=4)
 
 
-PINNED_CAP_GB = 64 * 2 ** 30 / 1e9   # pinned host memory one process may hold on the GPU machine (measured)
+PINNED_CAP_GB = 64 * 2 ** 30 / 1e9   # pinned host memory one process could hold on the test machine (measured)
 
 
 def test_full_size_qwen3_235b_slice_host_pool():
     """Qwen3-235B-A22B-shaped slice with its cold pool in pinned host memory.
 
-    The full 16-layer pool is 77.3 GB; the GPU machine lets one process pin at most
-    64 GiB, so the test keeps as many layers as fit (12: 58.0 GB), every other
-    dimension at full size."""
+    The full 16-layer pool is 77.3 GB; one process could pin at most 64 GiB of
+    host memory on the test machine, so the test keeps as many layers as fit
+    (12: 58.0 GB), every other dimension at full size."""
     w = synth.WORKLOADS["qwen3_235b_slice"]
     per_layer = w.N * w.expert_bytes / 1e9
     L = min(w.L, int(0.85 * PINNED_CAP_GB // per_layer))
