@@ -545,7 +545,6 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
             while (dw) {
                 const int b = __builtin_ctzll(dw);
                 dw &= dw - 1;
-                const int e = j * 64 + b;
                 if (count < lo.C) {
                     cw[j] |= 1ull << b;
                     ++count;

@@ -300,7 +300,7 @@ __device__ inline void up_heavy(const Layout& lo, int l, int ft, const int32_t* 
 // multiple of 64, so every wavefront has a tile).  W = 1: every wavefront
 // on its own; W = kWaves: grouped.
 template <int W>
-__global__ __launch_bounds__(64 * W) void ffn_up_bf16(Layout lo, int l, int bbuf, int sv,
+__global__ __launch_bounds__(64 * W) void ffn_up_bf16(Layout lo, int l, int bbuf, int /*sv: slots come with the units*/,
                                                       const uint16_t* __restrict__ h) {
     const int wgn = lo.F / (16 * W);
     const int u = blockIdx.x / wgn;
@@ -391,7 +391,7 @@ __device__ inline void down_heavy(const Layout& lo, int l, int dt, bool active, 
 
 // Workgroup (u, j): the W 32-row d-tiles W j + wavefront of unit u.
 template <int W>
-__global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bbuf, int sv) {
+__global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bbuf, int /*sv: slots come with the units*/) {
     const int dtn = lo.d / 32;
     const int wgn = (dtn + W - 1) / W;
     const int u = blockIdx.x / wgn;
