@@ -2,12 +2,15 @@
 // ("execute the MoE layer", Algorithm 2), grouped by expert:
 //   a_e = silu(W_gate,e x) * (W_up,e x),  y_(s,k) = g_(s,k) W_down,e a_e,
 //   y_s = sum_k y_(s,k)  (k in ascending order).
-// Each expert's weights are read once per layer step from its HBM slot,
-// whatever the number of tokens routed to it, so the layer step streams
-// |union of selected experts| x expert_bytes: the kernels are HBM-bound.
+// Each expert's weights are read from its HBM slot once per work unit (a
+// pass over up to 64 of its tokens; nearly every expert needs one), so the
+// layer step streams about |union of selected experts| x expert_bytes: the
+// kernels are HBM-bound.
 //
 // bf16: one wavefront per 16 rows of W_gate and of W_up (gate/up kernel) or
-// per 32 rows of W_down (down kernel), on the bf16 matrix core
+// per 32 rows of W_down (down kernel), one wavefront per workgroup or four
+// (grouped: consecutive row tiles of one unit, big units sharing their
+// activations through LDS), on the bf16 matrix core
 // (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  The expert's tokens form the
 // 16 columns of the B operand (groups of 16 tokens; several groups reuse the
 // loaded weights).  Per 64-wide k chunk, lane (r, g) of the A operand holds

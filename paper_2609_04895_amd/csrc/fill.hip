@@ -10,7 +10,8 @@
 // Every workgroup derives the same assignment from the same inputs (the
 // caches and the slot maps of version rv, which nobody writes during the
 // launch), then copies its share of the new experts; workgroup 0 also writes
-// the new slot maps (version rv ^ 1).  No workgroup waits for another, and
+// the new slot maps (version rv ^ 1) and, after the post-access update, lays
+// out the layer step's FFN work units.  No workgroup waits for another, and
 // the host never has to read the fill list.  The pool may be pinned host
 // memory mapped into the device; copies then run over the host link.
 #include "cmoe_internal.h"
