@@ -355,6 +355,22 @@ def main():
     print(f"[bench] {json.dumps(res)}", file=sys.stderr, flush=True)
     eng.cmoe_destroy()
     del inputs, hidden
+    if "roofline" in res:
+        # second reference: a plain 1 GiB device copy in the same process
+        # (bytes read + bytes written per second)
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for _ in range(5):
+            dst.copy_(src)
+        c1.record()
+        torch.cuda.synchronize()
+        copy_gbs = 5 * 2 * (1 << 30) / (c0.elapsed_time(c1) / 1e3) / 1e9
+        res["roofline"]["device_copy_GBs"] = copy_gbs
+        res["roofline"]["frac_of_device_copy"] = res["roofline"]["achieved"] / copy_gbs
+        del src, dst
     if args.calibrate_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")   # 1 GiB
         dst = torch.empty_like(src)
