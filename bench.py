@@ -378,7 +378,14 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if args.cpu_seconds > 0:
-        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        cb = cpu_baseline(w, args.cpu_seconds)
+        # the whole workload (S streams x T tokens x L layers) at the sampled
+        # rates: an extrapolation, not a measurement
+        full = w.S * w.T * w.L
+        cb["extrapolated_full_workload_s"] = {"one_core": full / cb["value"]}
+        if "all_cores" in cb:
+            cb["extrapolated_full_workload_s"]["all_cores"] = full / cb["all_cores"]["value"]
+        res["cpu_baseline"] = cb
     print(json.dumps(res), flush=True)
 
 
