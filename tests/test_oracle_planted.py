@@ -17,6 +17,7 @@ PRIM = ["tests/test_oracle_primitives.py"]
 METRIC = ["tests/test_oracle_metrics.py", "tests/test_oracle_replay.py"]
 POLICY = ["tests/test_oracle_policies.py"]
 CONC = ["tests/test_oracle_concentration.py"]
+GATES = ["tests/test_oracle_gates.py"]
 
 # (name, source text, replacement, pins expected to catch it)
 MISTAKES = [
@@ -50,6 +51,16 @@ MISTAKES = [
      "for (int k = 0; k < K - 1; ++k) st->selcount[(size_t)l * N + sel[k]] += 1;", CONC),
     ("highest free slot first", "for (int q = 0; q < st->n_slots && chosen < 0; ++q) {",
      "for (int q = st->n_slots - 1; q >= 0 && chosen < 0; --q) {", ["tests/test_oracle_replay.py"]),
+    ("softmax without the max shift", "float diff = z[e] - m;", "float diff = z[e];", PRIM),
+    ("Top-K prefers the higher index on ties", "if (best < 0 || v[e] > v[best]) best = e;",
+     "if (best < 0 || v[e] >= v[best]) best = e;", PRIM),
+    ("native bias dropped", "if (bias) acc += (double)bias[e];", "if (bias) acc += 0.0;", PRIM),
+    ("logits accumulated in fp32", "for (int i = 0; i < d; ++i) acc += (double)w[i] * (double)h[i];",
+     "for (int i = 0; i < d; ++i) acc = (float)(acc + (double)w[i] * (double)h[i]);", PRIM),
+    ("gates not renormalised", "out->gate[sl * K + k] = (double)pR[sel[k]] / gsum;",
+     "out->gate[sl * K + k] = (double)pR[sel[k]];", GATES),
+    ("refinement examines candidates from the lowest score up", "        int e = A[i];\n        if (C[e]) continue;",
+     "        int e = A[R - 1 - i];\n        if (C[e]) continue;", CACHE),
     ("residents give up their slots", "if (slot[e] >= 0 && !need[e]) slot[e] = -1;", "slot[e] = -1;",
      ["tests/test_oracle_replay.py"]),
 ]

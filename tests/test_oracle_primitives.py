@@ -86,6 +86,18 @@ def test_softmax_closed_forms():
     assert abs(p[0] - 0.75) < 3e-7 and abs(p[1] - 0.25) < 3e-7
 
 
+def test_softmax_is_exactly_shift_invariant():
+    # the max-shifted definition sees only z - max z; for logits on a 1/8 grid
+    # adding c keeps z + c - (max z + c) exact in fp32, so the results agree
+    # bit for bit (also where exp(z + c) itself would overflow)
+    rng = np.random.default_rng(13)
+    for n in (2, 5, 16, 128):
+        z = (rng.integers(-32, 33, size=n) / 8.0).astype(np.float32)
+        p = oracle.softmax(z)
+        for c in (64.0, 1000.0, -1000.0):
+            assert np.array_equal(oracle.softmax((z + np.float32(c)).astype(np.float32)), p), (n, c)
+
+
 def test_softmax_is_monotone():
     rng = np.random.default_rng(7)
     z = np.sort(rng.normal(size=128).astype(np.float32) * 3)
