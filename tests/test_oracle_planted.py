@@ -61,6 +61,10 @@ MISTAKES = [
      "out->gate[sl * K + k] = (double)pR[sel[k]];", GATES),
     ("refinement examines candidates from the lowest score up", "        int e = A[i];\n        if (C[e]) continue;",
      "        int e = A[R - 1 - i];\n        if (C[e]) continue;", CACHE),
+    ("down projection transposed", "acc += (double)wd[(size_t)j * F + f] * act[f];",
+     "acc += (double)wd[(size_t)f * d + j] * act[f];", PRIM),
+    ("up projection reads the gate weights", "b += (double)wu[(size_t)f * d + i] * (double)x[i];",
+     "b += (double)wg[(size_t)f * d + i] * (double)x[i];", PRIM),
     ("residents give up their slots", "if (slot[e] >= 0 && !need[e]) slot[e] = -1;", "slot[e] = -1;",
      ["tests/test_oracle_replay.py"]),
 ]

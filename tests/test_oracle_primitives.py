@@ -161,6 +161,29 @@ def test_moe_ffn_against_numpy_fp64():
     assert np.max(np.abs(y - ref)) <= 1e-12 * np.max(np.abs(ref))
 
 
+def test_moe_ffn_one_hot_weights_route_each_activation():
+    # x = e_2; row f of W_gate picks a_f, row f of W_up picks f + 1, and
+    # W_down sends activation f to output perm[f] alone:
+    # y[perm[f]] = g silu(a_f) (f + 1), every other output 0
+    d, F, g = 6, 5, 0.75
+    a = [0.5, -1.0, 2.0, 0.0, 1.5]
+    perm = [4, 0, 5, 1, 3]
+    x = np.zeros(d, np.float32)
+    x[2] = 1.0
+    Wg = np.zeros((1, F, d), np.float32)
+    Wu = np.zeros((1, F, d), np.float32)
+    Wd = np.zeros((1, d, F), np.float32)
+    for f in range(F):
+        Wg[0, f, 2] = a[f]
+        Wu[0, f, 2] = f + 1
+        Wd[0, perm[f], f] = 1.0
+    y = oracle.moe_ffn(Wg, Wu, Wd, [g], x)
+    expect = np.zeros(d)
+    for f in range(F):
+        expect[perm[f]] = g * a[f] / (1.0 + math.exp(-a[f])) * (f + 1)
+    assert np.allclose(y, expect, rtol=1e-15, atol=1e-300)
+
+
 def test_moe_ffn_closed_form_silu():
     # d = F = 1: W_gate = a, W_up = 1, W_down = 1, x = 1 -> y = g * silu(a)
     for a, silu in ((1.0, 0.7310585786300049), (-2.0, -0.2384058440442351), (0.0, 0.0)):
