@@ -53,6 +53,8 @@ CASES = [
     (2, 1, 1, 1, 1, 2, 1, 0, False, True),       # a single expert
     (2, 256, 8, 16, 4, 300, 1, 0, True, True),   # 1200 cache words per layer: several per fill thread
     (1, 32, 4, 8, 3, 5, 1, 0, True, True),       # one layer: its causal predecessor is itself, one token back
+    (2, 256, 64, 256, 256, 3, 1, 0, True, True),  # the largest N, K, C and R the kernels take
+    (2, 8, 2, 3, 2, 1000, 1, 0, True, True),      # 1000 streams over 8 experts: buckets of ~250 tokens
 ]
 
 

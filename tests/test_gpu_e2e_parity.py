@@ -188,3 +188,10 @@ def test_bf16_top11_output_combine():
     # a clamped batch of three, in k order
     w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_top11", L=2, N=32, K=11, d=128, F=64, S=12, C=16)
     run_e2e(w, T=6, tol=2e-2)
+
+
+def test_bf16_top64_largest_k():
+    # K = 64 (the largest Top-K): eight full batches in the output combine,
+    # 64 gated outputs per stream, every expert of a layer selected
+    w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_top64", L=2, N=64, K=64, d=128, F=64, S=5, C=64)
+    run_e2e(w, T=3, tol=2e-2)
