@@ -195,3 +195,11 @@ def test_bf16_top64_largest_k():
     # 64 gated outputs per stream, every expert of a layer selected
     w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_top64", L=2, N=64, K=64, d=128, F=64, S=5, C=64)
     run_e2e(w, T=3, tol=2e-2)
+
+
+@pytest.mark.parametrize("shape", ["single", "grouped"])
+def test_bf16_buckets_of_hundreds_of_tokens(shape):
+    # 600 streams over 4 experts, top-2: ~300 tokens per expert, so every
+    # bucket is cut into about five 64-token work units
+    w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_big_buckets", L=1, N=4, K=2, d=128, F=64, S=600, C=4, R=0)
+    run_e2e(w, T=3, tol=2e-2, ffn_shape=shape)
