@@ -373,6 +373,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.rw[1] = dv.iT == 1 ? w->w_temporal : (dv.iS == 1 ? w->w_spatio : nullptr);
     lo.rw[2] = dv.iS == 2 ? w->w_spatio : nullptr;
     lo.bias = w->logit_bias; lo.pool = pool_dev;
+    lo.pool_host = cfg->pool_kind == CMOE_POOL_HOST_PINNED ? 1 : 0;
     lo.arena = buf->arena;
     char* sb = static_cast<char*>(buf->state);
     char* wb = static_cast<char*>(buf->workspace);

@@ -32,6 +32,7 @@ struct Layout {
     const void* rw[3];
     const float* bias;
     const void* pool;
+    int32_t pool_host;     // 1: the pool is pinned host memory read over the host link
     // arena: [L][n_slots] experts
     void* arena;
     // state

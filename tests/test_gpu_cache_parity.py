@@ -170,16 +170,26 @@ def packed_from_plain(plain_u16, d, F):
     return np.concatenate(units)
 
 
-def test_bf16_slots_hold_the_packed_expert():
+@pytest.mark.parametrize("pool_kind,d,F", [("device", 128, 128), ("host", 128, 128), ("device", 192, 320),
+                                            ("host", 192, 320)])
+def test_bf16_slots_hold_the_packed_expert(pool_kind, d, F):
+    # the fill walks an HBM pool in packed-block order and a pinned host pool
+    # in source order; both must leave the same packed bytes in the slots
     from paper_2609_04895_amd import cmoe as B
-    L, N, K, C, S, d, F = 2, 8, 2, 3, 3, 128, 128
+    L, N, K, C, S = 2, 8, 2, 3, 3
+    say(f"packed slots, {pool_kind} pool, d={d} F={F}")
     dev = torch.device("cuda", 0)
     w = torch.zeros((L, N, d), dtype=torch.bfloat16, device=dev)
     per = 3 * d * F
     gen = torch.Generator().manual_seed(3)
     pool_cpu = torch.randint(0, 2 ** 16, (L, N, per), generator=gen, dtype=torch.int32).to(torch.int16)
-    pool = pool_cpu.view(torch.bfloat16).to(dev)
-    cfg = B.make_config(L, N, K, d, F, C, 0, S, 0, B.CMOE_BF16)
+    if pool_kind == "host":
+        pool = pool_cpu.view(torch.bfloat16).pin_memory()
+        kind = B.CMOE_POOL_HOST_PINNED
+    else:
+        pool = pool_cpu.view(torch.bfloat16).to(dev)
+        kind = B.CMOE_POOL_DEVICE
+    cfg = B.make_config(L, N, K, d, F, C, 0, S, 0, B.CMOE_BF16, kind)
     eng = B.Engine(cfg, w, w, None, None, pool)
     rng = np.random.default_rng(4)
     z = logits_sequence(rng, 5, S, L, N, ties=False)
