@@ -231,6 +231,7 @@ def main():
     ap.add_argument("--lrfu-lambda", type=float, default=None)
     ap.add_argument("--layers", type=int, default=None,
                     help="run the first L layers only (a pinned-host pool larger than the host allows)")
+    ap.add_argument("--streams", type=int, default=None, help="number of decode streams S (default: the workload's)")
     ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
     ap.add_argument("--ffn-shape", choices=["auto", "single", "grouped"], default="auto",
                     help="bf16 FFN workgroups: one wavefront each, or four sharing big units' activations "
@@ -267,6 +268,8 @@ def main():
         w = w.replace(lrfu_lambda=args.lrfu_lambda)
     if args.layers is not None:
         w = w.replace(L=args.layers)
+    if args.streams is not None:
+        w = w.replace(S=args.streams)
     warmup = args.warmup
     steps = args.steps if args.steps is not None else max(1, w.T - warmup)
     if args.overlap_study:
