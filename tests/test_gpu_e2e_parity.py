@@ -203,4 +203,3 @@ def test_bf16_buckets_of_hundreds_of_tokens(shape):
     # bucket is cut into about five 64-token work units
     w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_big_buckets", L=1, N=4, K=2, d=128, F=64, S=600, C=4, R=0)
     run_e2e(w, T=3, tol=2e-2, ffn_shape=shape)
-
