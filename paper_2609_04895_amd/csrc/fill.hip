@@ -267,7 +267,7 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
 }  // namespace
 
 hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st, const Timing& tm) {
-    launch_kernel(fill_kernel, dim3(kFillBlocks), dim3(256), st, tm, lo, f);
+    launch_kernel(fill_kernel, dim3(lo.pool_host ? kFillBlocksHost : kFillBlocksDevice), dim3(256), st, tm, lo, f);
     return hipGetLastError();
 }
 
