@@ -49,6 +49,16 @@ def compare_step(eng, run: oracle.Run, out: dict, where: str):
     if run.policy != oracle.POLICY_ROUTER:
         pol = eng.cmoe_read(B.CMOE_VIEW_PRIORITY)
         assert np.array_equal(pol.view(np.uint32), run.pol.view(np.uint32)), f"{where}: priorities differ"
+    # distinct experts selected per layer step, summed over the counted tokens
+    # (what bench.py's roofline counts as expert weight reads); compare_step
+    # runs after every token, so the sum is complete
+    if not hasattr(run, "active_expected"):
+        run.active_expected = np.zeros(run.L, np.int64)
+    if run.t - 1 >= run.cfg.warmup_tokens:
+        for l in range(run.L):
+            run.active_expected[l] += np.unique(out["sel"][:, l, :]).size
+    active = eng.cmoe_read(B.CMOE_VIEW_ACTIVE)
+    assert np.array_equal(active, run.active_expected), f"{where}: distinct experts per layer differ"
 
 
 def oracle_logits(w, WR, WT, WS, bias, H, t, streams):
