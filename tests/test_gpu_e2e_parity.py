@@ -203,3 +203,12 @@ def test_bf16_buckets_of_hundreds_of_tokens(shape):
     # bucket is cut into about five 64-token work units
     w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_big_buckets", L=1, N=4, K=2, d=128, F=64, S=600, C=4, R=0)
     run_e2e(w, T=3, tol=2e-2, ffn_shape=shape)
+
+
+def test_bf16_large_hidden_dims():
+    # d = 8192, F = 4096: 201 MB per expert, 128 k chunks per gate/up tile,
+    # router ranges at the largest split length
+    w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_large_dims", L=1, N=8, K=2, d=8192, F=4096, S=3, C=3, R=1,
+                                             mode=synth.MODE_SPATIO_TEMPORAL)
+    run_e2e(w, T=3, tol=2e-2)
+
