@@ -212,3 +212,12 @@ def test_bf16_large_hidden_dims():
                                              mode=synth.MODE_SPATIO_TEMPORAL)
     run_e2e(w, T=3, tol=2e-2)
 
+
+@pytest.mark.parametrize("shape", ["single", "grouped"])
+def test_bf16_two_thousand_streams(shape):
+    # 2048 streams over 16 experts, top-4: ~512 tokens per expert, eight work
+    # units each; 2048 cache-step workgroups and 4096 cache words per fill
+    w = synth.WORKLOADS["qwen3_30b"].replace(name="bf16_2048_streams", L=1, N=16, K=4, d=64, F=64, S=2048, C=6, R=2,
+                                             mode=synth.MODE_SPATIO_TEMPORAL)
+    run_e2e(w, T=3, tol=2e-2, ffn_shape=shape)
+
