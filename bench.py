@@ -120,22 +120,30 @@ def cpu_baseline(w, budget_s, max_threads=16):
         # every thread replays the same tokens from a fresh state, so it
         # selects the same experts, all generated above
         busy_t = [0.0] * threads
-        start = threading.Barrier(threads)
+        errors = []
+        start = threading.Barrier(threads, timeout=120)
 
         def replay(i):
-            r = new_run()
-            start.wait()
-            for t in range(tokens):
-                busy_t[i] += token(r, t, lambda l, e: experts[(l, e)])
+            try:
+                r = new_run()
+                start.wait()
+                for t in range(tokens):
+                    busy_t[i] += token(r, t, lambda l, e: experts[(l, e)])
+            except Exception as exc:  # reported below; a failed thread breaks the barrier for the others
+                errors.append(repr(exc))
+                start.abort()
 
         pool = [threading.Thread(target=replay, args=(i,)) for i in range(threads)]
         for th in pool:
             th.start()
         for th in pool:
             th.join()
-        res["all_cores"] = {"value": sum(tokens * w.L / b for b in busy_t), "cores": threads,
-                            "sample": f"{threads} threads at once, each replaying the {tokens} tokens above; "
-                                      f"{max(busy_t):.1f} s of oracle time per thread"}
+        if errors:
+            res["all_cores"] = {"error": errors[0]}
+        else:
+            res["all_cores"] = {"value": sum(tokens * w.L / b for b in busy_t), "cores": threads,
+                                "sample": f"{threads} threads at once, each replaying the {tokens} tokens above; "
+                                          f"{max(busy_t):.1f} s of oracle time per thread"}
     return res
 
 
@@ -386,7 +394,7 @@ def main():
         # rates: an extrapolation, not a measurement
         full = w.S * w.T * w.L
         cb["extrapolated_full_workload_s"] = {"one_core": full / cb["value"]}
-        if "all_cores" in cb:
+        if "value" in cb.get("all_cores", {}):
             cb["extrapolated_full_workload_s"]["all_cores"] = full / cb["all_cores"]["value"]
         res["cpu_baseline"] = cb
     print(json.dumps(res), flush=True)
