@@ -24,7 +24,9 @@
 // SwiGLU intermediate is stored in bf16 (the input type of the down kernel's
 // matrix core).
 //
-// fp32: plain VALU kernels, one thread per output row, fp32 accumulation.
+// fp32: VALU kernels, one lane per output row, fp32 accumulation, over
+// transposed weights (the fill kernel writes them so): the lanes of a
+// wavefront read consecutive floats for each k, 32 k at a time.
 #include "cmoe_internal.h"
 
 namespace cmoe {
@@ -430,6 +432,8 @@ __global__ __launch_bounds__(64) void ffn_up_f32(Layout lo, int l, int bbuf, int
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
     const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
     if (slot < 0 || slot >= lo.n_slots) return;
+    // transposed in the slot (the fill writes W_gate^T, W_up^T as [d][F]):
+    // the 64 lanes, rows f, read 64 consecutive floats per k
     const float* Wg = reinterpret_cast<const float*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems;
     const float* Wu = Wg + (int64_t)lo.F * lo.d;
     const int f = ft * 64 + threadIdx.x;
@@ -439,9 +443,19 @@ __global__ __launch_bounds__(64) void ffn_up_f32(Layout lo, int l, int bbuf, int
         const int s = pair >> 8;
         const float* x = h + ((int64_t)s * lo.L + l) * lo.d;
         float ag = 0.0f, au = 0.0f;
-        for (int i = 0; i < lo.d; ++i) {
-            ag = __builtin_fmaf(Wg[(int64_t)f * lo.d + i], x[i], ag);
-            au = __builtin_fmaf(Wu[(int64_t)f * lo.d + i], x[i], au);
+        for (int i0 = 0; i0 < lo.d; i0 += 32) {  // d is a multiple of 64
+            float wg[32], wu[32], xv[32];        // every load of a batch issued before the FMAs
+#pragma unroll
+            for (int u = 0; u < 32; ++u) {
+                wg[u] = Wg[(int64_t)(i0 + u) * lo.F + f];
+                wu[u] = Wu[(int64_t)(i0 + u) * lo.F + f];
+                xv[u] = x[i0 + u];
+            }
+#pragma unroll
+            for (int u = 0; u < 32; ++u) {
+                ag = __builtin_fmaf(wg[u], xv[u], ag);
+                au = __builtin_fmaf(wu[u], xv[u], au);
+            }
         }
         act[((int64_t)s * lo.K + (pair & 255)) * lo.F + f] = ag / (1.0f + expf(-ag)) * au;
     }
@@ -455,6 +469,7 @@ __global__ __launch_bounds__(64) void ffn_down_f32(Layout lo, int l, int bbuf, i
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
     const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
     if (slot < 0 || slot >= lo.n_slots) return;
+    // W_down^T [F][d] in the slot: lanes (rows j) read consecutive floats
     const float* Wd = reinterpret_cast<const float*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems +
                       2 * (int64_t)lo.F * lo.d;
     const int j = dt * 64 + threadIdx.x;
@@ -464,7 +479,16 @@ __global__ __launch_bounds__(64) void ffn_down_f32(Layout lo, int l, int bbuf, i
         const int s = pair >> 8, k = pair & 255;
         const float* av = act + ((int64_t)s * lo.K + k) * lo.F;
         float acc = 0.0f;
-        for (int f = 0; f < lo.F; ++f) acc = __builtin_fmaf(Wd[(int64_t)j * lo.F + f], av[f], acc);
+        for (int f0 = 0; f0 < lo.F; f0 += 32) {  // F is a multiple of 64
+            float wd[32], a32[32];
+#pragma unroll
+            for (int u = 0; u < 32; ++u) {
+                wd[u] = Wd[(int64_t)(f0 + u) * lo.d + j];
+                a32[u] = av[f0 + u];
+            }
+#pragma unroll
+            for (int u = 0; u < 32; ++u) acc = __builtin_fmaf(wd[u], a32[u], acc);
+        }
         const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
         lo.yp[((int64_t)s * lo.K + k) * lo.d + j] = gk * acc;
     }

@@ -259,7 +259,25 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
                 dst[(int64_t)b * 128 + packed_dest_in_block(w)] = src[m.src + (w >> 3) * m.row + (w & 7)];
             }
         } else {
-            for (int64_t i = gid; i < n16; i += gs) dst[i] = src[i];
+            // fp32: each matrix transposed (W_gate^T, W_up^T [d][F], W_down^T
+            // [F][d]) so that the lanes of the FFN kernels, one output row
+            // each, read consecutive addresses; walked in source order
+            const float* s32 = reinterpret_cast<const float*>(src);
+            float* d32 = reinterpret_cast<float*>(dst);
+            const int64_t dF = (int64_t)lo.d * lo.F;
+            for (int64_t i = gid; i < 3 * dF; i += gs) {
+                const int part = (int)(i / dF);
+                const int64_t r = i - part * dF;
+                int64_t o;
+                if (part < 2) {
+                    const int64_t f = r / lo.d, k = r - f * lo.d;  // W[f][k]
+                    o = part * dF + k * lo.F + f;
+                } else {
+                    const int64_t j = r / lo.F, f = r - j * lo.F;  // W_down[j][f]
+                    o = 2 * dF + f * lo.d + j;
+                }
+                d32[o] = s32[i];
+            }
         }
     }
 }

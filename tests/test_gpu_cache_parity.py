@@ -124,7 +124,9 @@ def test_refinement_budget_change_and_cache_set_replay():
 
 
 def test_fills_copy_the_right_expert_bytes():
-    """Arena slots hold exactly the cold-pool bytes of the expert mapped there."""
+    """Arena slots hold exactly the cold-pool values of the expert mapped
+    there, each fp32 matrix transposed (W_gate^T, W_up^T [d][F], then
+    W_down^T [F][d])."""
     L, N, K, C, S = 2, 16, 2, 4, 3
     rng = np.random.default_rng(8)
     z = logits_sequence(rng, 6, S, L, N, ties=False)
@@ -138,11 +140,16 @@ def test_fills_copy_the_right_expert_bytes():
     n_slots = min(N, S * C)
     per = 3 * 64 * 64
     arena = eng.arena[: L * n_slots * per * 4].view(torch.float32).reshape(L, n_slots, per)
+    d = F = 64
     for l in range(L):
         for e in range(N):
             q = int(slots[l, e])
             if q >= 0:
-                assert torch.equal(arena[l, q], pool[l, e]), (l, e, q)
+                src = pool[l, e]
+                want = torch.cat([src[:F * d].reshape(F, d).t().reshape(-1),
+                                  src[F * d:2 * F * d].reshape(F, d).t().reshape(-1),
+                                  src[2 * F * d:].reshape(d, F).t().reshape(-1)])
+                assert torch.equal(arena[l, q], want), (l, e, q)
     eng.cmoe_destroy()
 
 
