@@ -3,10 +3,18 @@ from __future__ import annotations
 
 import copy
 import sys
+import zlib
 
 import numpy as np
 
 import oracle
+
+
+def stable_seed(text: str) -> int:
+    """A seed derived from a test-case name that is the same in every process
+    (str hashes are salted per process, so hash() would draw new inputs on
+    every run and a failing case could not be replayed from its ID)."""
+    return zlib.crc32(text.encode("ascii"))
 
 
 def say(*a):

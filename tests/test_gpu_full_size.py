@@ -128,8 +128,10 @@ def test_full_size_gptoss_20b_full_mode():
     run_full(synth.WORKLOADS["gptoss_20b"], T=24)
 
 
-@pytest.mark.parametrize("C,R", [(16, 0), (32, 2), (64, 4)])
+@pytest.mark.parametrize("C,R", [(C, R) for C in (16, 32, 64) for R in (0, 2, 4)])
 def test_full_size_qwen3_30b_zipf_sweep_points(C, R):
+    """Every (C, R) point of the Zipf workload's capacity x refinement-budget
+    sweep (the stand-in for Table 3's sweep)."""
     run_full(synth.WORKLOADS["qwen3_30b_zipf"].replace(C=C, R=R), T=10, ffn_samples=4)
 
 

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import compare_step, say
+from gpu_util import compare_step, say, stable_seed
 from test_gpu_cache_parity import logits_sequence
 
 pytestmark = pytest.mark.gpu
@@ -56,9 +56,11 @@ def test_random_config_cache_path_bit_exact(case):
     from paper_2609_04895_amd import cmoe as B
     c = case
     L, N, K, C, R, S, mode, policy = c["L"], c["N"], c["K"], c["C"], c["R"], c["S"], c["mode"], c["policy"]
-    say(f"random config {case_id(c)} lam={c['lam']} warmup={c['warmup']} ties={c['ties']} side={c['side']}")
+    seed = stable_seed(case_id(c))
+    say(f"random config {case_id(c)} seed={seed} lam={c['lam']} warmup={c['warmup']} ties={c['ties']} "
+        f"side={c['side']}")
     T = 8
-    rng = np.random.default_rng(abs(hash(case_id(c))) % (2 ** 32))
+    rng = np.random.default_rng(seed)
     z = logits_sequence(rng, T, S, L, N, c["ties"])
     dev = torch.device("cuda", 0)
     d = F = 64
