@@ -165,7 +165,11 @@ cmoe_status cmoe_query(const cmoe_config* cfg, cmoe_sizes* out);
 
 /* Binds weights and buffers, clears the state (empty caches, zero counters, no
  * resident experts) on main_stream and returns a handle.  side_stream may be
- * NULL (then fills run on main_stream).  Streams are hipStream_t values. */
+ * NULL (then fills run on main_stream).  Streams are hipStream_t values.
+ * buf->workspace may be NULL for a handle that runs every token through
+ * cmoe_step_noalloc; its per-step buffers must then fit the scratch array
+ * (CMOE_ERR_UNSUPPORTED otherwise).  The handle belongs to the device that is
+ * current during this call. */
 cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_buffers* buf,
                       void* main_stream, void* side_stream, cmoe_handle** out);
 
@@ -174,6 +178,21 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
  * y: [S][L][d] fp32 output of each MoE layer (device), valid once main_stream
  *    has completed.  The token index t is kept by the handle. */
 cmoe_status cmoe_step(cmoe_handle* hd, const void* h, float* y);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): cmoe_step
+ * with the per-step buffers (router partials, logits, selections, gates,
+ * buckets, work units, the SwiGLU intermediate and the gated expert outputs)
+ * in a scratch array that the library holds on each device, 64 MiB, instead
+ * of the handle's workspace.  Allocates nothing; the same kernels, inputs,
+ * outputs and results as cmoe_step.  Every call on a device shares that
+ * device's array and leaves its contents behind (each call clears what must
+ * start at zero); calls that overlap in time on one device race, so calls of
+ * different handles must be ordered (one stream, or synchronized).  The views
+ * of per-token outputs then read the scratch array until the next cmoe_step.
+ * CMOE_ERR_UNSUPPORTED when the configuration's per-step buffers exceed
+ * 64 MiB; CMOE_ERR_INVALID_ARG when the current device is not the handle's. */
+cmoe_status cmoe_step_noalloc(cmoe_handle* hd, const void* h, float* y);
 
 /* The cache path of one token from given fp32 logits, without the router
  * GEMV and without the FFN: softmax, Top-K, refinement, access, retention,

@@ -52,7 +52,7 @@ CMOE_VIEW_SELCOUNT = 11
 CMOE_KERNEL_COUNT = 6
 KERNEL_NAMES = ("router", "cache_step", "fill", "ffn_up", "ffn_down", "combine")
 
-EXPORTED = ("cmoe_query", "cmoe_init", "cmoe_step", "cmoe_step_logits", "cmoe_stats", "cmoe_get_cache",
+EXPORTED = ("cmoe_query", "cmoe_init", "cmoe_step", "cmoe_step_noalloc", "cmoe_step_logits", "cmoe_stats", "cmoe_get_cache",
             "cmoe_set_cache", "cmoe_set_R", "cmoe_reset", "cmoe_destroy", "cmoe_view_bytes", "cmoe_read",
             "cmoe_profile_begin", "cmoe_profile_end", "cmoe_concentration", "cmoe_last_error")
 
@@ -106,6 +106,7 @@ def lib():
         L.cmoe_init.argtypes = [ctypes.POINTER(cmoe_config), ctypes.POINTER(cmoe_weights),
                                 ctypes.POINTER(cmoe_buffers), vp, vp, ctypes.POINTER(vp)]
         L.cmoe_step.argtypes = [vp, vp, vp]
+        L.cmoe_step_noalloc.argtypes = [vp, vp, vp]
         L.cmoe_step_logits.argtypes = [vp, vp, vp, vp]
         L.cmoe_stats.argtypes = [vp, ctypes.POINTER(cmoe_stats_t), i64p, i64p]
         L.cmoe_get_cache.argtypes = [vp, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
@@ -162,7 +163,9 @@ class Engine:
     """One handle plus the caller-owned buffers (torch tensors on cuda:0)."""
 
     def __init__(self, cfg: cmoe_config, w_router, w_temporal, w_spatio, logit_bias, cold_pool,
-                 main_stream=None, side_stream=None):
+                 main_stream=None, side_stream=None, workspace=True):
+        """workspace=False binds no workspace: every token then goes through
+        cmoe_step_noalloc."""
         import torch
         self.torch = torch
         self.cfg = cfg
@@ -175,12 +178,12 @@ class Engine:
 
         self.arena = buf(sizes.arena_bytes)
         self.state = buf(sizes.state_bytes)
-        self.workspace = buf(sizes.workspace_bytes)
+        self.workspace = buf(sizes.workspace_bytes) if workspace else None
         self._keep = (w_router, w_temporal, w_spatio, logit_bias, cold_pool)
         self.main_stream = main_stream if main_stream is not None else torch.cuda.current_stream()
         self.side_stream = side_stream
         wts = cmoe_weights(_ptr(w_router), _ptr(w_temporal), _ptr(w_spatio), _ptr(logit_bias), _ptr(cold_pool))
-        bufs = cmoe_buffers(_ptr(self.arena), _ptr(self.state), _ptr(self.workspace))
+        bufs = cmoe_buffers(_ptr(self.arena), _ptr(self.state), _ptr(self.workspace) if workspace else None)
         h = ctypes.c_void_p()
         _check(lib().cmoe_init(ctypes.byref(cfg), ctypes.byref(wts), ctypes.byref(bufs),
                                ctypes.c_void_p(self.main_stream.cuda_stream),
@@ -191,6 +194,9 @@ class Engine:
     # -- the decode path
     def cmoe_step(self, h, y):
         _check(lib().cmoe_step(self.handle, ctypes.c_void_p(h.data_ptr()), ctypes.c_void_p(y.data_ptr())))
+
+    def cmoe_step_noalloc(self, h, y):
+        _check(lib().cmoe_step_noalloc(self.handle, ctypes.c_void_p(h.data_ptr()), ctypes.c_void_p(y.data_ptr())))
 
     def cmoe_step_logits(self, zR, zT=None, zS=None):
         _check(lib().cmoe_step_logits(self.handle, ctypes.c_void_p(zR.data_ptr()), ctypes.c_void_p(_ptr(zT)),

@@ -624,23 +624,34 @@ __global__ void init_kernel(Layout lo) {
     }
     for (int64_t i = gid; i < (int64_t)lo.S * lo.N; i += gs) lo.pS[i] = 0.0f;
     for (int64_t i = gid; i < (int64_t)lo.S * lo.L * kNctr; i += gs) lo.ctr[i] = 0;
-    for (int64_t i = gid; i < (int64_t)lo.L * 2; i += gs) {
-        lo.phys[i] = 0;
-        lo.step_fills[i] = 0;
-    }
+    for (int64_t i = gid; i < (int64_t)lo.L * 2; i += gs) lo.phys[i] = 0;
     for (int64_t i = gid; i < lo.L; i += gs) lo.active_sum[i] = 0ull;
     for (int64_t i = gid; i < (int64_t)lo.L * lo.N; i += gs) lo.selcount[i] = 0ull;
     for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.N; i += gs) lo.slot_of[i] = -1;
     for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.n_slots; i += gs) lo.slot_exp[i] = -1;
+    if (lo.events == nullptr) return;  // no workspace bound (kernel-uniform)
+    for (int64_t i = gid; i < (int64_t)lo.L * 2; i += gs) lo.step_fills[i] = 0;
     for (int64_t i = gid; i < (int64_t)lo.L * lo.S * 4; i += gs) lo.events[i] = 0;
     for (int64_t i = gid; i < (int64_t)2 * lo.N; i += gs) lo.bcount[i] = 0;
     for (int64_t i = gid; i < lo.N; i += gs) lo.zero_row[i] = 0.0f;
+}
+
+// What a token's first layer step needs zero in a workspace that other calls
+// may have left behind: both bucket-count buffers and the zero bias row.
+__global__ __launch_bounds__(256) void prep_workspace_kernel(Layout lo) {
+    for (int i = threadIdx.x; i < 2 * lo.N; i += blockDim.x) lo.bcount[i] = 0;
+    for (int i = threadIdx.x; i < lo.N; i += blockDim.x) lo.zero_row[i] = 0.0f;
 }
 
 }  // namespace
 
 hipError_t launch_init(const Layout& lo, hipStream_t st) {
     hipLaunchKernelGGL(init_kernel, dim3(256), dim3(256), 0, st, lo);
+    return hipGetLastError();
+}
+
+hipError_t launch_prep_workspace(const Layout& lo, hipStream_t st) {
+    hipLaunchKernelGGL(prep_workspace_kernel, dim3(1), dim3(256), 0, st, lo);
     return hipGetLastError();
 }
 

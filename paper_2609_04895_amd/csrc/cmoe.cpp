@@ -19,6 +19,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -29,9 +30,35 @@ using cmoe::FillArgs;
 using cmoe::Layout;
 using cmoe::StepArgs;
 
+// Per-step scratch of cmoe_step_noalloc, for callers that cannot allocate a
+// workspace: one array per GPU, loaded with the library and held until the
+// process ends.  In host code `scratch` names a host-side stand-in, never the
+// device memory: the device address comes from hipGetSymbolAddress, taken once
+// per device at cmoe_init with that device current.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
 
 thread_local std::string g_err;
+
+std::mutex g_scratch_mu;
+std::vector<void*> g_scratch_ptr;  // device address of `scratch` on each device, once resolved
+
+// The device address of the scratch array on the current device `dev`.
+hipError_t scratch_on_device(int dev, void** out) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (dev >= (int)g_scratch_ptr.size()) g_scratch_ptr.resize(dev + 1, nullptr);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 cmoe_status fail(cmoe_status st, const std::string& msg) {
     g_err = msg;
@@ -159,13 +186,36 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     return p;
 }
 
+// Points the workspace members of lo into the buffer wb (nullptr: none).
+void bind_workspace(Layout& lo, char* wb, const Plan& p) {
+    auto at = [wb](size_t off) -> char* { return wb ? wb + off : nullptr; };
+    lo.zpart = reinterpret_cast<double*>(at(p.zpart));
+    lo.logits = reinterpret_cast<float*>(at(p.logits));
+    lo.sel = reinterpret_cast<int32_t*>(at(p.sel));
+    lo.gates = reinterpret_cast<float*>(at(p.gates));
+    lo.events = reinterpret_cast<int32_t*>(at(p.events));
+    lo.step_fills = reinterpret_cast<int32_t*>(at(p.step_fills));
+    lo.bcount = reinterpret_cast<int32_t*>(at(p.bcount));
+    lo.pairs = reinterpret_cast<int32_t*>(at(p.pairs));
+    lo.act = at(p.act);
+    lo.yp = reinterpret_cast<float*>(at(p.yp));
+    lo.zero_row = reinterpret_cast<float*>(at(p.zero_row));
+    lo.units = reinterpret_cast<int32_t*>(at(p.units));
+}
+
 }  // namespace
 
 struct cmoe_handle {
     cmoe_config cfg;
     Derived dv;
     Plan plan;
-    Layout lo;
+    Layout lo;                  // workspace pointers into the caller's workspace (null if none was given)
+    Layout lo_static;           // the same with workspace pointers into the device's scratch array
+    const Layout* cur = nullptr;  // the layout of the token being launched
+    bool has_ws = false;        // the caller bound a workspace
+    bool scratch_fits = false;  // the workspace plan fits the scratch array
+    bool last_static = false;   // the last token ran on the scratch array
+    int device = 0;
     hipStream_t main = nullptr, side = nullptr;
     bool side_is_main = true;
     std::vector<hipEvent_t> ev_access, ev_pro;
@@ -221,18 +271,28 @@ hipError_t timed(cmoe_handle* hd, int kid, F&& launch) {
 hipError_t fill(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, hipStream_t st, int bbuf = -1) {
     FillArgs f{layer, kind, hd->ver[layer], counted ? 1 : 0, zero_pre ? 1 : 0, bbuf};
     hd->ver[layer] ^= 1;
-    return timed(hd, KID_FILL, [&](const cmoe::Timing& tm) { return cmoe::launch_fill(hd->lo, f, st, tm); });
+    return timed(hd, KID_FILL, [&](const cmoe::Timing& tm) { return cmoe::launch_fill(*hd->cur, f, st, tm); });
 }
 
 // One decode token.  h == nullptr selects injected logits (no router, no FFN).
-cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR, const float* zT, const float* zS) {
+// on_scratch: the per-step buffers are the device's scratch array instead of
+// the caller's workspace.
+cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR, const float* zT, const float* zS,
+                      bool on_scratch = false) {
     const cmoe_config& c = hd->cfg;
-    const Layout& lo = hd->lo;
+    hd->cur = on_scratch ? &hd->lo_static : &hd->lo;
+    const Layout& lo = *hd->cur;
     const bool inject = h == nullptr;
     const bool refine_on = has_spatio(c.mode) && hd->t >= 1 && hd->R > 0;
     const bool counted = hd->t >= c.warmup_tokens;
     const uint32_t count = counted ? cmoe::kFlagCount : 0u;
     hipStream_t M = hd->main, Sd = hd->side;
+
+    // A workspace that other calls used last may hold nonzero bucket counts:
+    // the scratch array always (other handles share it), the caller's
+    // workspace after tokens that ran on the scratch array.
+    if (on_scratch || hd->last_static) HIPCHK(cmoe::launch_prep_workspace(lo, M), "workspace preparation");
+    hd->last_static = on_scratch;
 
     if (refine_on) {  // layer 0: refined from the previous token's last-layer prediction
         StepArgs a{0, 0, hd->R, 0, cmoe::kFlagRefine | count, hd->t, {nullptr, nullptr, nullptr}};
@@ -327,10 +387,27 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
         return fail(CMOE_ERR_INVALID_ARG, "w_temporal is required with the router policy");
     if (dv.iS > 0 && !w->w_spatio)
         return fail(CMOE_ERR_INVALID_ARG, "w_spatio is required in the modes with a Spatio Router");
-    if (!buf->arena || !buf->state || !buf->workspace)
-        return fail(CMOE_ERR_INVALID_ARG, "arena, state and workspace buffers are required");
+    if (!buf->arena || !buf->state) return fail(CMOE_ERR_INVALID_ARG, "arena and state buffers are required");
     for (const void* p : {buf->arena, buf->state, buf->workspace})
         if (reinterpret_cast<uintptr_t>(p) & 255) return fail(CMOE_ERR_INVALID_ARG, "buffers must be 256-byte aligned");
+    const Plan plan = make_plan(cfg, dv);
+    if (!buf->workspace && plan.ws_total > kScratchBytes)
+        return fail(CMOE_ERR_UNSUPPORTED, "no workspace given and the per-step buffers (" +
+                                              std::to_string(plan.ws_total) + " bytes) exceed the " +
+                                              std::to_string(kScratchBytes) + "-byte scratch array");
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(CMOE_ERR_HIP, "hipGetDevice failed");
+    }
+    void* scratch_dev = nullptr;
+    {
+        const hipError_t e = scratch_on_device(device, &scratch_dev);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(CMOE_ERR_HIP, std::string("hipGetSymbolAddress of the scratch array: ") + hipGetErrorString(e));
+        }
+    }
 
     // The fill kernel reads the cold pool directly: resolve its device address
     // (a pinned host pool must be hipHostMalloc memory) and refuse pointers the
@@ -354,7 +431,10 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     cmoe_handle* hd = new cmoe_handle();
     hd->cfg = *cfg;
     hd->dv = dv;
-    hd->plan = make_plan(cfg, dv);
+    hd->plan = plan;
+    hd->device = device;
+    hd->has_ws = buf->workspace != nullptr;
+    hd->scratch_fits = plan.ws_total <= kScratchBytes;
     hd->R = has_spatio(cfg->mode) ? cfg->R : 0;
     hd->ver.assign(cfg->L, 0);
     hd->main = static_cast<hipStream_t>(main_stream);
@@ -376,7 +456,6 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.pool_host = cfg->pool_kind == CMOE_POOL_HOST_PINNED ? 1 : 0;
     lo.arena = buf->arena;
     char* sb = static_cast<char*>(buf->state);
-    char* wb = static_cast<char*>(buf->workspace);
     lo.cache = reinterpret_cast<unsigned long long*>(sb + p.cache);
     lo.aT = reinterpret_cast<float*>(sb + p.aT);
     lo.pol = reinterpret_cast<float*>(sb + p.pol);
@@ -387,20 +466,12 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.selcount = reinterpret_cast<unsigned long long*>(sb + p.selcount);
     lo.slot_of = reinterpret_cast<int32_t*>(sb + p.slot_of);
     lo.slot_exp = reinterpret_cast<int32_t*>(sb + p.slot_exp);
-    lo.zpart = reinterpret_cast<double*>(wb + p.zpart);
-    lo.logits = reinterpret_cast<float*>(wb + p.logits);
-    lo.sel = reinterpret_cast<int32_t*>(wb + p.sel);
-    lo.gates = reinterpret_cast<float*>(wb + p.gates);
-    lo.events = reinterpret_cast<int32_t*>(wb + p.events);
-    lo.step_fills = reinterpret_cast<int32_t*>(wb + p.step_fills);
-    lo.bcount = reinterpret_cast<int32_t*>(wb + p.bcount);
-    lo.pairs = reinterpret_cast<int32_t*>(wb + p.pairs);
-    lo.act = wb + p.act;
-    lo.yp = reinterpret_cast<float*>(wb + p.yp);
-    lo.zero_row = reinterpret_cast<float*>(wb + p.zero_row);
-    lo.units = reinterpret_cast<int32_t*>(wb + p.units);
     lo.max_units = max_units(cfg);
     lo.ffn_waves = dv.ffn_waves;
+    hd->lo_static = lo;
+    bind_workspace(lo, static_cast<char*>(buf->workspace), p);
+    bind_workspace(hd->lo_static, hd->scratch_fits ? static_cast<char*>(scratch_dev) : nullptr, p);
+    hd->cur = &hd->lo;
 
     auto mk = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
     hd->ev_access.resize(cfg->L);
@@ -424,12 +495,30 @@ cmoe_status cmoe_step(cmoe_handle* hd, const void* h, float* y) {
     cmoe_status st = usable(hd);
     if (st != CMOE_OK) return st;
     if (!h || !y) return fail(CMOE_ERR_INVALID_ARG, "h and y are required");
+    if (!hd->has_ws) return fail(CMOE_ERR_INVALID_ARG, "the handle has no workspace: use cmoe_step_noalloc");
     return run_token(hd, h, y, nullptr, nullptr, nullptr);
+}
+
+cmoe_status cmoe_step_noalloc(cmoe_handle* hd, const void* h, float* y) {
+    cmoe_status st = usable(hd);
+    if (st != CMOE_OK) return st;
+    if (!h || !y) return fail(CMOE_ERR_INVALID_ARG, "h and y are required");
+    if (!hd->scratch_fits)
+        return fail(CMOE_ERR_UNSUPPORTED, "the per-step buffers (" + std::to_string(hd->plan.ws_total) +
+                                              " bytes) exceed the " + std::to_string(kScratchBytes) +
+                                              "-byte scratch array: use cmoe_step with a workspace");
+    int device = -1;
+    if (hipGetDevice(&device) != hipSuccess || device != hd->device) {
+        (void)hipGetLastError();
+        return fail(CMOE_ERR_INVALID_ARG, "the current device is not the one the handle was created on");
+    }
+    return run_token(hd, h, y, nullptr, nullptr, nullptr, true);
 }
 
 cmoe_status cmoe_step_logits(cmoe_handle* hd, const float* zR, const float* zT, const float* zS) {
     cmoe_status st = usable(hd);
     if (st != CMOE_OK) return st;
+    if (!hd->has_ws) return fail(CMOE_ERR_INVALID_ARG, "the handle has no workspace: use cmoe_step_noalloc");
     if (!zR) return fail(CMOE_ERR_INVALID_ARG, "zR is required");
     if (hd->dv.iT > 0 && !zT) return fail(CMOE_ERR_INVALID_ARG, "zT is required with the router policy");
     if (hd->dv.iS > 0 && !zS) return fail(CMOE_ERR_INVALID_ARG, "zS is required in the modes with a Spatio Router");
@@ -573,7 +662,9 @@ cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t byte
     const size_t need = cmoe_view_bytes(hd, view);
     if (need == 0) return fail(CMOE_ERR_INVALID_ARG, "unknown view");
     if (!host_out || bytes < need) return fail(CMOE_ERR_INVALID_ARG, "output buffer too small");
-    const Layout& lo = hd->lo;
+    // per-token outputs live where the last token ran
+    const Layout& lo = (hd->last_static || !hd->has_ws) ? hd->lo_static : hd->lo;
+    if (!lo.events) return fail(CMOE_ERR_STATE, "no per-step buffers to read");
     st = sync_all(hd);
     if (st != CMOE_OK) return st;
     if (view == CMOE_VIEW_SLOTS) {  // the current version of each layer's slot map

@@ -111,7 +111,8 @@ inline void launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipSt
         hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
 }
 
-hipError_t launch_init(const Layout& lo, hipStream_t st);
+hipError_t launch_init(const Layout& lo, hipStream_t st);  // state, and the workspace if bound
+hipError_t launch_prep_workspace(const Layout& lo, hipStream_t st);
 hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st, const Timing& tm = {});
 hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st, const Timing& tm = {});
 hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st, const Timing& tm = {});

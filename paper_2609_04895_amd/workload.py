@@ -18,9 +18,9 @@ def config_for(w, C: Optional[int] = None, R: Optional[int] = None, warmup_token
 
 
 def engine_for(w, inputs, C: Optional[int] = None, R: Optional[int] = None, warmup_tokens: int = 0,
-               side_stream: bool = True, ffn_shape: Optional[str] = None):
+               side_stream: bool = True, ffn_shape: Optional[str] = None, workspace: bool = True):
     import torch
     cfg = config_for(w, C, R, warmup_tokens, fill_on_main=not side_stream, ffn_shape=ffn_shape)
     side = torch.cuda.Stream() if side_stream else None
     return Engine(cfg, inputs["wR"], inputs.get("wT"), inputs.get("wS"), inputs.get("bias"), inputs["pool"],
-                  side_stream=side)
+                  side_stream=side, workspace=workspace)
