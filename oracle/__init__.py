@@ -39,7 +39,8 @@ class _Cfg(ctypes.Structure):
 
 class _State(ctypes.Structure):
     _fields_ = [("cache", _u8p), ("aT", _f32p), ("pS", _f32p), ("ctr", _i64p), ("slot_of", _i32p),
-                ("phys", _i64p), ("pol", _f32p), ("selcount", _i64p), ("n_slots", ctypes.c_int32),
+                ("phys", _i64p), ("pol", _f32p), ("selcount", _i64p), ("stamp", _i64p), ("clk", _i64p),
+                ("n_slots", ctypes.c_int32),
                 ("t", ctypes.c_int32)]
 
 
@@ -195,9 +196,12 @@ class Run:
 
     mode: MODE_TEMPORAL (update-only), MODE_SPATIO_TEMPORAL (full) or
     MODE_SPATIO_ONLY; policy: POLICY_ROUTER (s^T) or a classical retention
-    priority (LRU, LFU, LRFU with ``lrfu_lambda``)."""
+    priority (LRU, LFU, LRFU with ``lrfu_lambda``); arena_slots: physical
+    slots per layer (0: min(N, S C), which always holds the union of the
+    caches)."""
 
-    def __init__(self, L, N, K, C, R, S, mode, warmup_tokens=0, policy=POLICY_ROUTER, lrfu_lambda=0.5):
+    def __init__(self, L, N, K, C, R, S, mode, warmup_tokens=0, policy=POLICY_ROUTER, lrfu_lambda=0.5,
+                 arena_slots=0):
         self.cfg = _Cfg(L, N, K, C, R, S, mode, warmup_tokens, policy, lrfu_weight(lrfu_lambda))
         self.L, self.N, self.K, self.C, self.S, self.mode = L, N, K, C, S, mode
         self.policy = policy
@@ -209,7 +213,9 @@ class Run:
         self.ctr = np.zeros((S, L, NCTR), dtype=np.int64)
         self.slot_of = np.full((L, N), -1, dtype=np.int32)
         self.phys = np.zeros((L, 2), dtype=np.int64)
-        self.n_slots = min(N, S * C)
+        self.stamp = np.zeros((L, N), dtype=np.int64)
+        self.clk = np.zeros(L, dtype=np.int64)
+        self.n_slots = arena_slots if arena_slots else min(N, S * C)
         self.t = 0
 
     @property
@@ -222,7 +228,7 @@ class Run:
     def _state(self):
         return _State(_p(self.cache, _u8p), _p(self.aT, _f32p), _p(self.pS, _f32p), _p(self.ctr, _i64p),
                       _p(self.slot_of, _i32p), _p(self.phys, _i64p), _p(self.pol, _f32p), _p(self.selcount, _i64p),
-                      self.n_slots, self.t)
+                      _p(self.stamp, _i64p), _p(self.clk, _i64p), self.n_slots, self.t)
 
     def step(self, zR, zT=None, zS=None, want=("sel", "gate")):
         """zR, zT, zS: [S][L][N] float32 (zT only for the router policy in the

@@ -47,6 +47,16 @@
  *     caches in numbered slots; a newly needed expert takes the lowest free
  *     slot, in ascending expert order.  Refinement and the post-access update
  *     each end with such a residency event.
+ *   - A capacity-limited arena (fewer slots per layer than the union of the
+ *     caches can reach, the paper's bounded device cache taken literally for
+ *     many streams) is a second-level cache over the slots: when the union
+ *     fits it behaves as above; when it does not, the layer step's executed
+ *     experts pass through the slots in rounds of at most n_slots experts
+ *     (the experts already resident first, then the others, each group in
+ *     ascending order), every missing expert taking the lowest free slot or
+ *     else evicting the least recently used expert that no remaining round
+ *     needs (lower slot on equal recency), and refinement only fills free
+ *     slots.
  *   - Classical priorities live per (stream, layer, expert) and are updated
  *     once per access, before the eviction decision: LRU stores the time of
  *     the last use (0 = never), LFU the number of selections, LRFU
@@ -348,6 +358,10 @@ typedef struct {
     int64_t* phys;    /* [L][2]    physical fills: demand, proactive (counted)  */
     float* pol;       /* [S][L][N] classical retention priority (policy != 0)  */
     int64_t* selcount;/* [L][N]    native selections per expert (counted tokens) */
+    int64_t* stamp;   /* [L][N]    physical recency: the arena clock at the last
+                                    use of each expert's copy (valid while resident) */
+    int64_t* clk;     /* [L]       arena clock: advances once per round of a
+                                    residency event                              */
     int32_t n_slots;  /* physical slots per layer                              */
     int32_t t;        /* index of the next token                               */
 } orc_state;
@@ -364,34 +378,97 @@ typedef struct {      /* optional per-token outputs (any pointer may be NULL) */
     int32_t* fills;   /* [L][2] physical fills of this token: demand, proactive */
 } orc_out;
 
-/* Residency event: the layer must now hold the union of the streams' caches.
- * Experts that left the union free their slots; each newly needed expert, in
- * ascending order, takes the lowest free slot.  Returns the number of fills. */
-static int orc_residency(const orc_cfg* c, orc_state* st, int l) {
+/* Lowest free slot of a layer's arena, or -1 when every slot is taken. */
+static int orc_free_slot(const orc_state* st, int N, const int32_t* slot) {
+    for (int q = 0; q < st->n_slots; ++q) {
+        int used = 0;
+        for (int u = 0; u < N; ++u)
+            if (slot[u] == q) used = 1;
+        if (!used) return q;
+    }
+    return -1;
+}
+
+/* Residency event of layer l.  U is the union of the streams' caches;
+ * experts that left U free their slots.  E: the experts the layer step's FFN
+ * executes (after the post-access update), or NULL (after refinement).
+ *   - U fits the slots: every member of U becomes resident, each new one, in
+ *     ascending order, in the lowest free slot.
+ *   - U does not fit, after refinement: new members of U, in ascending order,
+ *     take free slots while there are any.
+ *   - U does not fit, after the post-access update: E is ordered, resident
+ *     experts first, then the others, each group ascending, and executed in
+ *     rounds of n_slots consecutive experts.  In its round each missing
+ *     expert, in that order, takes the lowest free slot, or else the slot of
+ *     the resident expert that no remaining round needs with the oldest last
+ *     use (lower slot on ties), which is evicted.
+ * The clock advances once per round (once in the first two cases); every
+ * expert copied, and every expert executed in a round, gets it as its last
+ * use.  Returns the number of copies. */
+static int orc_residency(const orc_cfg* c, orc_state* st, int l, const uint8_t* E) {
     const int N = c->N;
-    uint8_t need[ORC_NMAX];
-    memset(need, 0, (size_t)N);
+    uint8_t inU[ORC_NMAX];
+    memset(inU, 0, (size_t)N);
     for (int s = 0; s < c->S; ++s) {
         const uint8_t* cs = st->cache + ((size_t)s * c->L + l) * N;
         for (int e = 0; e < N; ++e)
-            if (cs[e]) need[e] = 1;
+            if (cs[e]) inU[e] = 1;
     }
     int32_t* slot = st->slot_of + (size_t)l * N;
+    int64_t* stamp = st->stamp + (size_t)l * N;
     for (int e = 0; e < N; ++e)
-        if (slot[e] >= 0 && !need[e]) slot[e] = -1;
+        if (slot[e] >= 0 && !inU[e]) slot[e] = -1;
+    const int nU = orc_count(inU, N);
     int fills = 0;
-    for (int e = 0; e < N; ++e) {
-        if (!need[e] || slot[e] >= 0) continue;
-        int chosen = -1;
-        for (int q = 0; q < st->n_slots && chosen < 0; ++q) {
-            int used = 0;
-            for (int u = 0; u < N; ++u)
-                if (slot[u] == q) used = 1;
-            if (!used) chosen = q;
+    if (nU <= st->n_slots || !E) {
+        const int64_t now = ++st->clk[l];
+        for (int e = 0; e < N; ++e) {
+            if (!inU[e] || slot[e] >= 0) continue;
+            const int q = orc_free_slot(st, N, slot);
+            if (q < 0) {
+                if (nU <= st->n_slots) return -1; /* cannot happen: the union fits */
+                break;                            /* refinement: no free slot left */
+            }
+            slot[e] = q;
+            stamp[e] = now;
+            ++fills;
         }
-        if (chosen < 0) return -1; /* cannot happen: union <= n_slots */
-        slot[e] = chosen;
-        ++fills;
+        if (E)
+            for (int e = 0; e < N; ++e)
+                if (E[e]) stamp[e] = now;
+        return fills;
+    }
+    int32_t order[ORC_NMAX], round_of[ORC_NMAX];
+    int nE = 0;
+    for (int e = 0; e < N; ++e)
+        if (E[e] && slot[e] >= 0) order[nE++] = e;
+    for (int e = 0; e < N; ++e)
+        if (E[e] && slot[e] < 0) order[nE++] = e;
+    for (int e = 0; e < N; ++e) round_of[e] = -1;
+    for (int i = 0; i < nE; ++i) round_of[order[i]] = i / st->n_slots;
+    for (int r = 0; r * st->n_slots < nE; ++r) {
+        const int64_t now = ++st->clk[l];
+        const int lo = r * st->n_slots, hi = lo + st->n_slots < nE ? lo + st->n_slots : nE;
+        for (int i = lo; i < hi; ++i) {
+            const int e = order[i];
+            if (slot[e] >= 0) continue;
+            int q = orc_free_slot(st, N, slot);
+            if (q < 0) {
+                int victim = -1;
+                for (int v = 0; v < N; ++v) {
+                    if (slot[v] < 0 || round_of[v] >= r) continue; /* absent, or needed now or later */
+                    if (victim < 0 || stamp[v] < stamp[victim] ||
+                        (stamp[v] == stamp[victim] && slot[v] < slot[victim]))
+                        victim = v;
+                }
+                if (victim < 0) return -1; /* cannot happen: a round fits the slots */
+                q = slot[victim];
+                slot[victim] = -1;
+            }
+            slot[e] = q;
+            ++fills;
+        }
+        for (int i = lo; i < hi; ++i) stamp[order[i]] = now;
     }
     return fills;
 }
@@ -448,7 +525,7 @@ int orc_step(const orc_cfg* c, orc_state* st, const float* zR, const float* zT, 
                 if (out && out->nP) out->nP[sl] = nP;
                 if (out && out->sST) memcpy(out->sST + sl * N, sST, sizeof(float) * (size_t)N);
             }
-            int f = orc_residency(c, st, l);
+            int f = orc_residency(c, st, l, NULL);
             if (f < 0) return -1;
             if (counted) st->phys[(size_t)l * 2 + 1] += f;
             if (out && out->fills) out->fills[l * 2 + 1] = f;
@@ -459,10 +536,13 @@ int orc_step(const orc_cfg* c, orc_state* st, const float* zR, const float* zT, 
             if (out && out->fills) out->fills[l * 2 + 1] = 0;
         }
         /* Native routing, access, post-access retention (Algorithm 1). */
+        uint8_t executed[ORC_NMAX];   /* experts this layer step's FFN executes */
+        memset(executed, 0, (size_t)N);
         for (int s = 0; s < S; ++s) {
             const size_t sl = (size_t)s * L + l;
             orc_softmax(zR + sl * N, N, pR);
             orc_topk(zR + sl * N, N, K, sel);
+            for (int k = 0; k < K; ++k) executed[sel[k]] = 1;
             double gsum = 0.0;
             for (int k = 0; k < K; ++k) gsum += (double)pR[sel[k]];
             if (router_policy) {
@@ -505,7 +585,7 @@ int orc_step(const orc_cfg* c, orc_state* st, const float* zR, const float* zT, 
                 if (out->nD) out->nD[sl] = nD;
             }
         }
-        int f = orc_residency(c, st, l);
+        int f = orc_residency(c, st, l, executed);
         if (f < 0) return -1;
         if (counted) st->phys[(size_t)l * 2 + 0] += f;
         if (out && out->fills) out->fills[l * 2 + 0] = f;

@@ -25,7 +25,7 @@ def say(*a):
 def clone_run(run: oracle.Run) -> oracle.Run:
     r = copy.copy(run)
     r.cfg = oracle._Cfg(*[getattr(run.cfg, n) for n, _ in oracle._Cfg._fields_])
-    for n in ("cache", "aT", "pS", "ctr", "slot_of", "phys", "pol", "selcount"):
+    for n in ("cache", "aT", "pS", "ctr", "slot_of", "phys", "pol", "selcount", "stamp", "clk"):
         setattr(r, n, getattr(run, n).copy())
     return r
 

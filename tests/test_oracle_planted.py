@@ -18,6 +18,7 @@ METRIC = ["tests/test_oracle_metrics.py", "tests/test_oracle_replay.py"]
 POLICY = ["tests/test_oracle_policies.py"]
 CONC = ["tests/test_oracle_concentration.py"]
 GATES = ["tests/test_oracle_gates.py"]
+ARENA = ["tests/test_oracle_arena.py"]
 
 # (name, source text, replacement, pins expected to catch it)
 MISTAKES = [
@@ -49,8 +50,8 @@ MISTAKES = [
      "for (int i = 0; i <= top_m && i < N; ++i) {", CONC),
     ("selection counts drop one expert", "for (int k = 0; k < K; ++k) st->selcount[(size_t)l * N + sel[k]] += 1;",
      "for (int k = 0; k < K - 1; ++k) st->selcount[(size_t)l * N + sel[k]] += 1;", CONC),
-    ("highest free slot first", "for (int q = 0; q < st->n_slots && chosen < 0; ++q) {",
-     "for (int q = st->n_slots - 1; q >= 0 && chosen < 0; --q) {", ["tests/test_oracle_replay.py"]),
+    ("highest free slot first", "for (int q = 0; q < st->n_slots; ++q) {",
+     "for (int q = st->n_slots - 1; q >= 0; --q) {", ["tests/test_oracle_replay.py"]),
     ("softmax without the max shift", "float diff = z[e] - m;", "float diff = z[e];", PRIM),
     ("Top-K prefers the higher index on ties", "if (best < 0 || v[e] > v[best]) best = e;",
      "if (best < 0 || v[e] >= v[best]) best = e;", PRIM),
@@ -65,8 +66,26 @@ MISTAKES = [
      "acc += (double)wd[(size_t)f * d + j] * act[f];", PRIM),
     ("up projection reads the gate weights", "b += (double)wu[(size_t)f * d + i] * (double)x[i];",
      "b += (double)wg[(size_t)f * d + i] * (double)x[i];", PRIM),
-    ("residents give up their slots", "if (slot[e] >= 0 && !need[e]) slot[e] = -1;", "slot[e] = -1;",
+    ("residents give up their slots", "if (slot[e] >= 0 && !inU[e]) slot[e] = -1;", "slot[e] = -1;",
      ["tests/test_oracle_replay.py"]),
+    ("arena evicts the most recently used", "if (victim < 0 || stamp[v] < stamp[victim] ||",
+     "if (victim < 0 || stamp[v] > stamp[victim] ||", ARENA),
+    ("arena evicts the higher slot on equal recency", "(stamp[v] == stamp[victim] && slot[v] < slot[victim]))",
+     "(stamp[v] == stamp[victim] && slot[v] > slot[victim]))", ARENA),
+    # (evicting an expert only a later round needs is not a distinct mistake:
+    # with resident experts executed first, no round that must evict has a
+    # resident expert left for a later round)
+    ("arena evicts an expert its own round needs", "if (slot[v] < 0 || round_of[v] >= r) continue;",
+     "if (slot[v] < 0 || round_of[v] > r) continue;", ARENA),
+    ("arena rounds start with the missing experts",
+     "        if (E[e] && slot[e] >= 0) order[nE++] = e;\n    for (int e = 0; e < N; ++e)\n"
+     "        if (E[e] && slot[e] < 0) order[nE++] = e;",
+     "        if (E[e] && slot[e] < 0) order[nE++] = e;\n    for (int e = 0; e < N; ++e)\n"
+     "        if (E[e] && slot[e] >= 0) order[nE++] = e;", ARENA),
+    ("executed experts keep their old recency", "                if (E[e]) stamp[e] = now;",
+     "                if (E[e]) stamp[e] = stamp[e];", ARENA),
+    ("arena rounds leave recency unchanged", "for (int i = lo; i < hi; ++i) stamp[order[i]] = now;",
+     "for (int i = lo; i < hi; ++i) stamp[order[i]] = stamp[order[i]];", ARENA),
 ]
 
 
