@@ -60,9 +60,13 @@ def describe(w):
     mode = {0: f"update-only, {retention} retention", 1: f"full Spatio-Temporal, R={w.R}",
             2: f"Spatio-only, R={w.R}, {retention} retention"}[w.mode]
     dt = "bf16" if w.dtype == 1 else "fp32"
-    return (f"{w.name}: L={w.L} N={w.N} K={w.K} d={w.d} SwiGLU {w.d}->{w.F}->{w.d} C={w.C} {mode}, "
+    import synth
+    base_L = synth.WORKLOADS[w.name].L if w.name in synth.WORKLOADS else w.L
+    layers = f"L={w.L}" if w.L == base_L else f"L={w.L} (the first {w.L} of its {base_L} layers)"
+    return (f"{w.name}: {layers} N={w.N} K={w.K} d={w.d} SwiGLU {w.d}->{w.F}->{w.d} C={w.C} {mode}, "
             f"{w.S} streams x {w.T} tokens, {dt}, AR(1) rho={w.rho}"
-            + (f", Zipf({w.zipf}) bias" if w.zipf else ""))
+            + (f", Zipf({w.zipf}) bias" if w.zipf else "")
+            + (f", {w.arena_slots} HBM expert slots per layer" if w.arena_slots else ""))
 
 
 def cpu_baseline(w, budget_s, max_procs=16):
@@ -287,6 +291,8 @@ def main():
     ap.add_argument("--lrfu-lambda", type=float, default=None)
     ap.add_argument("--layers", type=int, default=None, help="run the first L layers only")
     ap.add_argument("--streams", type=int, default=None, help="number of decode streams S (default: the workload's)")
+    ap.add_argument("--arena-slots", type=int, default=None,
+                    help="HBM expert slots per layer (default 0: min(N, S C), which holds the union of the caches)")
     ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
     ap.add_argument("--ffn-shape", choices=["auto", "single", "grouped"], default="auto",
                     help="bf16 FFN workgroups: one wavefront each, or four sharing big units' activations "
@@ -322,6 +328,8 @@ def main():
         w = w.replace(L=args.layers)
     if args.streams is not None:
         w = w.replace(S=args.streams)
+    if args.arena_slots is not None:
+        w = w.replace(arena_slots=args.arena_slots)
     warmup = args.warmup
     steps = args.steps if args.steps is not None else max(1, w.T - warmup)
     if args.overlap_study:
@@ -401,7 +409,8 @@ def main():
                    "capacity": w.C, "refine_budget": w.R if w.has_spatio else 0,
                    "mode": {0: "update-only", 1: "spatio-temporal", 2: "spatio-only"}[w.mode],
                    "retention": {v: k for k, v in POLICIES.items()}[w.policy], "d": w.d, "F": w.F,
-                   "fills": "main stream" if args.fill_on_main else "side stream", "ffn_shape": args.ffn_shape},
+                   "fills": "main stream" if args.fill_on_main else "side stream", "ffn_shape": args.ffn_shape,
+                   "arena_slots": w.arena_slots or min(w.N, w.S * w.C)},
     }
     # algorithmic bytes of one token step: each distinct selected expert read
     # once, router weights, hidden states in, layer outputs out, fills (read +
@@ -411,6 +420,10 @@ def main():
                   + 2 * tot["phys_bytes"]) / steps
     res["step_hbm"] = {"algorithmic_bytes": step_bytes, "achieved_GBs": step_bytes / (elapsed / steps) / 1e9,
                        "frac": step_bytes / (elapsed / steps) / 1e9 / HBM_PEAK_GBS}
+    if w.pool_kind == synth.POOL_HOST_PINNED:
+        # expert copies out of the pinned host pool cross the host link
+        res["host_link"] = {"copied_bytes_per_step": tot["phys_bytes"] / steps,
+                            "achieved_GBs": tot["phys_bytes"] / elapsed / 1e9}
     if passes == 2:
         # the same number of tokens again, each gate/up launch carrying a HIP
         # event pair that takes the kernel's own start and end timestamps

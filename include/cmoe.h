@@ -106,8 +106,21 @@ typedef enum {
 /* Problem shape.  Valid values: 1 <= K <= C <= N (Section 2: capacity at least
  * Top-K); 0 <= R <= N; L, S >= 1; d, F >= 1; warmup_tokens >= 0; a known mode
  * and policy, paired as cmoe_policy states; lrfu_lambda finite and >= 0 with
- * CMOE_POLICY_LRFU.  Supported: N <= 256, d and F multiples of 64.  R is
- * ignored in CMOE_MODE_TEMPORAL. */
+ * CMOE_POLICY_LRFU; 0 <= arena_slots <= min(N, S C).  Supported: N <= 256, d
+ * and F multiples of 64.  R is ignored in CMOE_MODE_TEMPORAL.
+ *
+ * Physical residency.  Each layer's HBM arena has arena_slots expert slots
+ * (0: min(N, S C), which always holds the union of the streams' caches).
+ * While the union of the caches fits, the arena holds all of it: an expert
+ * that leaves every cache frees its slot, a new one takes the lowest free slot
+ * (ascending expert order), after refinement and after the post-access update.
+ * When it does not fit (the paper's bounded device cache, Section 3.1 and the
+ * Figure 1 caption, with more streams than slots), the arena is a second-level
+ * cache: the layer step's FFN runs in rounds of at most arena_slots of the
+ * experts it executes (those already resident first, then the others, each
+ * group in ascending order); a missing expert takes the lowest free slot or
+ * evicts the least recently used expert that no remaining round needs (lower
+ * slot on equal recency); after refinement only free slots are filled. */
 typedef struct {
     int32_t L, N, K, d, F, C, R, S;
     int32_t mode;          /* cmoe_mode                                         */
@@ -118,6 +131,7 @@ typedef struct {
     uint32_t flags;
     int32_t policy;        /* cmoe_policy                                       */
     float lrfu_lambda;     /* LRFU recency weight (the paper uses 0.5)          */
+    int32_t arena_slots;   /* HBM expert slots per layer; 0: min(N, S C)        */
 } cmoe_config;
 
 /* Weights (device pointers unless stated).  Router matrices are bias-free
@@ -138,7 +152,7 @@ typedef struct {
 
 /* Device buffer sizes in bytes; every buffer must be 256-byte aligned. */
 typedef struct {
-    size_t arena_bytes;     /* HBM expert slots: L x min(N, S C) experts         */
+    size_t arena_bytes;     /* HBM expert slots: L x arena_slots experts         */
     size_t state_bytes;     /* caches, scores, counters, slot maps               */
     size_t workspace_bytes; /* per-step scratch and the inspectable outputs      */
 } cmoe_sizes;

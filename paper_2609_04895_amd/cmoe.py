@@ -60,7 +60,8 @@ EXPORTED = ("cmoe_query", "cmoe_init", "cmoe_step", "cmoe_step_noalloc", "cmoe_s
 class cmoe_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("L", "N", "K", "d", "F", "C", "R", "S", "mode", "dtype",
                                               "pool_kind", "warmup_tokens")] + \
-        [("flags", ctypes.c_uint32), ("policy", ctypes.c_int32), ("lrfu_lambda", ctypes.c_float)]
+        [("flags", ctypes.c_uint32), ("policy", ctypes.c_int32), ("lrfu_lambda", ctypes.c_float),
+         ("arena_slots", ctypes.c_int32)]
 
 
 class cmoe_weights(ctypes.Structure):
@@ -135,8 +136,9 @@ def _check(status: int):
 
 
 def make_config(L, N, K, d, F, C, R, S, mode, dtype, pool_kind=CMOE_POOL_DEVICE, warmup_tokens=0, flags=0,
-                policy=CMOE_POLICY_ROUTER, lrfu_lambda=0.5):
-    return cmoe_config(L, N, K, d, F, C, R, S, mode, dtype, pool_kind, warmup_tokens, flags, policy, lrfu_lambda)
+                policy=CMOE_POLICY_ROUTER, lrfu_lambda=0.5, arena_slots=0):
+    return cmoe_config(L, N, K, d, F, C, R, S, mode, dtype, pool_kind, warmup_tokens, flags, policy, lrfu_lambda,
+                       arena_slots)
 
 
 def router_slots(cfg: cmoe_config):

@@ -628,7 +628,10 @@ __global__ void init_kernel(Layout lo) {
     for (int64_t i = gid; i < lo.L; i += gs) lo.active_sum[i] = 0ull;
     for (int64_t i = gid; i < (int64_t)lo.L * lo.N; i += gs) lo.selcount[i] = 0ull;
     for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.N; i += gs) lo.slot_of[i] = -1;
-    for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.n_slots; i += gs) lo.slot_exp[i] = -1;
+    for (int64_t i = gid; i < (int64_t)2 * lo.L * lo.n_slots; i += gs) {
+        lo.slot_exp[i] = -1;
+        lo.slot_stamp[i] = 0;
+    }
     if (lo.events == nullptr) return;  // no workspace bound (kernel-uniform)
     for (int64_t i = gid; i < (int64_t)lo.L * 2; i += gs) lo.step_fills[i] = 0;
     for (int64_t i = gid; i < (int64_t)lo.L * lo.S * 4; i += gs) lo.events[i] = 0;

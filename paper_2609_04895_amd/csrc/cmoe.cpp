@@ -71,6 +71,7 @@ enum KernelId { KID_ROUTER = 0, KID_CACHE = 1, KID_FILL = 2, KID_UP = 3, KID_DOW
 
 struct Derived {
     int NW, n_r, n_slots, nsplit, rdk, zstride;
+    int rounds;        // FFN rounds per layer step: more than one only for an arena smaller than the union
     int iT, iS;        // router slots of the Temporal / Spatio Router, -1 if not used
     int ffn_waves;     // wavefronts per bf16 FFN workgroup (1 or 4)
     size_t esz, expert_bytes;
@@ -99,6 +100,9 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     if (c->pool_kind != CMOE_POOL_DEVICE && c->pool_kind != CMOE_POOL_HOST_PINNED)
         return fail(CMOE_ERR_INVALID_ARG, "unknown pool kind");
     if (c->warmup_tokens < 0) return fail(CMOE_ERR_INVALID_ARG, "warmup_tokens must be >= 0");
+    const int64_t max_slots = std::min<int64_t>(c->N, (int64_t)c->S * c->C);
+    if (c->arena_slots < 0 || c->arena_slots > max_slots)
+        return fail(CMOE_ERR_INVALID_ARG, "arena_slots must be in [0, min(N, S C)]");
     if (c->N > cmoe::kMaxN) return fail(CMOE_ERR_UNSUPPORTED, "N > 256 is not supported");
     if (c->K > cmoe::kMaxK) return fail(CMOE_ERR_UNSUPPORTED, "K > 64 is not supported");
     if (c->d % 64 || c->F % 64) return fail(CMOE_ERR_UNSUPPORTED, "d and F must be multiples of 64");
@@ -115,7 +119,11 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     dv->iT = temporal ? 1 : -1;
     dv->iS = has_spatio(c->mode) ? (temporal ? 2 : 1) : -1;
     dv->n_r = 1 + (temporal ? 1 : 0) + (has_spatio(c->mode) ? 1 : 0);
-    dv->n_slots = (int)std::min<int64_t>(c->N, (int64_t)c->S * c->C);
+    dv->n_slots = c->arena_slots ? c->arena_slots : (int)max_slots;
+    // the executed experts of a layer step (at most min(N, S K)) pass through a
+    // smaller arena in rounds of n_slots
+    const int64_t max_exec = std::min<int64_t>(c->N, (int64_t)c->S * c->K);
+    dv->rounds = dv->n_slots < max_slots ? (int)((max_exec + dv->n_slots - 1) / dv->n_slots) : 1;
     dv->esz = c->dtype == CMOE_BF16 ? 2 : 4;
     dv->expert_bytes = (size_t)3 * c->d * c->F * dv->esz;
     // router split-K: each wavefront of a router workgroup sums a 32-aligned
@@ -139,8 +147,8 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
 
 // Offsets of every sub-buffer; used both for sizing and for carving.
 struct Plan {
-    size_t cache, aT, pol, pS, ctr, phys, active_sum, selcount, slot_of, slot_exp, state_total;
-    size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, zero_row, units, ws_total;
+    size_t cache, aT, pol, pS, ctr, phys, active_sum, selcount, slot_of, slot_exp, slot_stamp, state_total;
+    size_t zpart, logits, sel, gates, events, step_fills, bcount, pairs, act, yp, zero_row, units, round_of, ws_total;
     size_t arena;
 };
 
@@ -167,6 +175,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.selcount = take(L * N * 8);
     p.slot_of = take(2 * L * N * 4);
     p.slot_exp = take(2 * L * (size_t)dv.n_slots * 4);
+    p.slot_stamp = take(2 * L * (size_t)dv.n_slots * 4);
     p.state_total = o;
     o = 0;
     p.zpart = take(S * dv.n_r * N * (size_t)dv.zstride * 8);
@@ -181,6 +190,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.yp = take(S * K * (size_t)c->d * 4);
     p.zero_row = take(N * 4);
     p.units = take((size_t)max_units(c) * 16);
+    p.round_of = take(N * 4);
     p.ws_total = o;
     p.arena = L * (size_t)dv.n_slots * dv.expert_bytes;
     return p;
@@ -201,6 +211,7 @@ void bind_workspace(Layout& lo, char* wb, const Plan& p) {
     lo.yp = reinterpret_cast<float*>(at(p.yp));
     lo.zero_row = reinterpret_cast<float*>(at(p.zero_row));
     lo.units = reinterpret_cast<int32_t*>(at(p.units));
+    lo.round_of = reinterpret_cast<int32_t*>(at(p.round_of));
 }
 
 }  // namespace
@@ -222,6 +233,7 @@ struct cmoe_handle {
     int32_t t = 0;            // next token
     int64_t g = 0;            // layer steps accessed so far (bucket buffer parity)
     std::vector<int> ver;     // current slot-map version of each layer
+    std::vector<int32_t> clk; // arena clock of each layer: advances once per fill launch
     int32_t R = 0;
     bool broken = false;
     // profiling
@@ -266,10 +278,12 @@ hipError_t timed(cmoe_handle* hd, int kid, F&& launch) {
     return launch(tm);
 }
 
-// One residency event of `layer` on stream st; advances the layer's slot-map
-// version.
-hipError_t fill(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, hipStream_t st, int bbuf = -1) {
-    FillArgs f{layer, kind, hd->ver[layer], counted ? 1 : 0, zero_pre ? 1 : 0, bbuf};
+// One residency event of `layer` (or one FFN round of it) on stream st;
+// advances the layer's slot-map version and arena clock.
+hipError_t fill(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, hipStream_t st, int bbuf = 0,
+                bool units = false, int round = 0) {
+    FillArgs f{layer, kind, hd->ver[layer], counted ? 1 : 0, zero_pre ? 1 : 0, bbuf, units ? 1 : 0, round,
+               ++hd->clk[layer]};
     hd->ver[layer] ^= 1;
     return timed(hd, KID_FILL, [&](const cmoe::Timing& tm) { return cmoe::launch_fill(*hd->cur, f, st, tm); });
 }
@@ -324,29 +338,36 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
         HIPCHK(timed(hd, KID_CACHE, [&](const cmoe::Timing& tm) { return cmoe::launch_cache_step(lo, a, M, tm); }),
                "cache step");
         hd->g += 1;
-        // demand loads gate this layer's FFN; the same launch lays out the FFN work units
-        HIPCHK(fill(hd, l, 0, counted, !refine_on, M, inject ? -1 : bbuf), "fill");
-        if (refine_next) {
-            if (hd->side_is_main) {
-                HIPCHK(fill(hd, l + 1, 1, counted, false, M), "fill");
-            } else {
-                HIPCHK(hipEventRecord(hd->ev_access[l], M), "event record");
-                HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[l], 0), "stream wait");
-                HIPCHK(fill(hd, l + 1, 1, counted, false, Sd), "fill");
-                HIPCHK(hipEventRecord(hd->ev_pro[l + 1], Sd), "event record");
+        // demand loads gate this layer's FFN; the same launch lays out the FFN
+        // work units.  An arena smaller than the union of the caches runs the
+        // FFN in rounds, each after the fill that brings its experts in.
+        for (int r = 0; r < hd->dv.rounds; ++r) {
+            HIPCHK(fill(hd, l, 0, counted, r == 0 && !refine_on, M, bbuf, !inject, r), "fill");
+            if (r == 0 && refine_next) {
+                if (hd->side_is_main) {
+                    HIPCHK(fill(hd, l + 1, 1, counted, false, M), "fill");
+                } else {
+                    HIPCHK(hipEventRecord(hd->ev_access[l], M), "event record");
+                    HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[l], 0), "stream wait");
+                    HIPCHK(fill(hd, l + 1, 1, counted, false, Sd), "fill");
+                    HIPCHK(hipEventRecord(hd->ev_pro[l + 1], Sd), "event record");
+                }
+            }
+            if (!inject) {
+                const int sv = hd->ver[l];
+                HIPCHK(timed(hd, KID_UP,
+                             [&](const cmoe::Timing& tm) {
+                                 return cmoe::launch_ffn_up(lo, l, bbuf, sv, r, h, M, tm);
+                             }),
+                       "ffn up");
+                HIPCHK(timed(hd, KID_DOWN,
+                             [&](const cmoe::Timing& tm) { return cmoe::launch_ffn_down(lo, l, bbuf, sv, r, M, tm); }),
+                       "ffn down");
             }
         }
-        if (!inject) {
-            const int sv = hd->ver[l];
-            HIPCHK(timed(hd, KID_UP,
-                         [&](const cmoe::Timing& tm) { return cmoe::launch_ffn_up(lo, l, bbuf, sv, h, M, tm); }),
-                   "ffn up");
-            HIPCHK(timed(hd, KID_DOWN,
-                         [&](const cmoe::Timing& tm) { return cmoe::launch_ffn_down(lo, l, bbuf, sv, M, tm); }),
-                   "ffn down");
+        if (!inject)
             HIPCHK(timed(hd, KID_COMBINE, [&](const cmoe::Timing& tm) { return cmoe::launch_combine(lo, l, y, M, tm); }),
                    "combine");
-        }
     }
     hd->t += 1;
     if (hd->prof_left > 0) hd->prof_left -= 1;
@@ -437,6 +458,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     hd->scratch_fits = plan.ws_total <= kScratchBytes;
     hd->R = has_spatio(cfg->mode) ? cfg->R : 0;
     hd->ver.assign(cfg->L, 0);
+    hd->clk.assign(cfg->L, 0);
     hd->main = static_cast<hipStream_t>(main_stream);
     hd->side_is_main = side_stream == nullptr || side_stream == main_stream || (cfg->flags & CMOE_FLAG_FILL_ON_MAIN);
     hd->side = hd->side_is_main ? hd->main : static_cast<hipStream_t>(side_stream);
@@ -466,6 +488,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.selcount = reinterpret_cast<unsigned long long*>(sb + p.selcount);
     lo.slot_of = reinterpret_cast<int32_t*>(sb + p.slot_of);
     lo.slot_exp = reinterpret_cast<int32_t*>(sb + p.slot_exp);
+    lo.slot_stamp = reinterpret_cast<int32_t*>(sb + p.slot_stamp);
     lo.max_units = max_units(cfg);
     lo.ffn_waves = dv.ffn_waves;
     hd->lo_static = lo;
@@ -617,6 +640,7 @@ cmoe_status cmoe_reset(cmoe_handle* hd) {
     hd->t = 0;
     hd->g = 0;
     hd->ver.assign(hd->cfg.L, 0);
+    hd->clk.assign(hd->cfg.L, 0);
     return CMOE_OK;
 }
 
@@ -700,7 +724,7 @@ cmoe_status cmoe_profile_begin(cmoe_handle* hd, int32_t max_tokens, uint32_t ker
     hd->prof_mask = kernel_mask ? kernel_mask : ((1u << CMOE_KERNEL_COUNT) - 1u);
     int kinds = 0;
     for (int k = 0; k < CMOE_KERNEL_COUNT; ++k) kinds += (hd->prof_mask >> k) & 1u;
-    const size_t per_token = ((size_t)hd->cfg.L * 2 + 2) * kinds;  // timed launches per token, upper bound
+    const size_t per_token = ((size_t)hd->cfg.L * (hd->dv.rounds + 1) + 2) * kinds;  // timed launches per token, at most
     const size_t need = 2 * per_token * (size_t)max_tokens;
     while (hd->prof_pool.size() < need) {
         hipEvent_t e;

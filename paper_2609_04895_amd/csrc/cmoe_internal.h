@@ -50,6 +50,7 @@ struct Layout {
     unsigned long long* selcount;    // [L][N] native selections per expert (counted tokens)
     int32_t* slot_of;           // [2][L][N]   slot of each expert, -1 absent (two versions)
     int32_t* slot_exp;          // [2][L][n_slots] expert in each slot, -1 free
+    int32_t* slot_stamp;        // [2][L][n_slots] arena clock at the last use of each slot's expert
     // workspace
     double* zpart;              // [S][n_r][N][zstride] router partial sums
     float* logits;              // [L][S][n_r][N]
@@ -62,9 +63,11 @@ struct Layout {
     void* act;                  // [S][K][F]   SwiGLU intermediate (dtype)
     float* yp;                  // [S][K][d]   gated expert outputs
     float* zero_row;            // [N]         zeros (native bias when there is none)
-    int32_t* units;             // [max_units][4] FFN work units of the layer step, heaviest
+    int32_t* units;             // [max_units][4] FFN work units of the current round, heaviest
                                 //             first: {(pass << 8) | expert, slot, tokens, 0},
                                 //             {-1, -1, 0, 0} past the end
+    int32_t* round_of;          // [N]         FFN round of each expert executed by the layer
+                                //             step, -1 if not executed
 };
 
 // cache-step kernel flags
@@ -84,15 +87,20 @@ struct StepArgs {
     const float* z[3];  // injected logits [S][L][N] per router slot (kFlagInject)
 };
 
-// One residency event: layer `layer` must hold the union of the streams'
-// caches.  Slot maps are read from version rv and written to version rv ^ 1.
+// One residency event of layer `layer` (or one round of it): the arena must
+// hold the union of the streams' caches, or, when the union does not fit,
+// the experts of this FFN round.  Slot maps and stamps are read from version
+// rv and written to version rv ^ 1.
 struct FillArgs {
     int32_t layer;
     int32_t kind;        // 0 after the post-access update, 1 after refinement
     int32_t rv;
     int32_t counted;
     int32_t zero_pre;    // kind 0: no refinement happened this token, clear its fill count
-    int32_t bbuf;        // kind 0: bucket buffer of the layer step (builds the FFN work units)
+    int32_t bbuf;        // kind 0: bucket buffer of the layer step (its counts give the executed experts)
+    int32_t units;       // kind 0: lay out the FFN work units of this round
+    int32_t round;       // kind 0: FFN round of the layer step (0 plans the rounds)
+    int32_t clk;         // arena clock of this launch: the last use it stamps
 };
 
 // Optional timing of one launch: with events, they take the kernel's own
@@ -116,9 +124,10 @@ hipError_t launch_prep_workspace(const Layout& lo, hipStream_t st);
 hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st, const Timing& tm = {});
 hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st, const Timing& tm = {});
 hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st, const Timing& tm = {});
-hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st,
+hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, int round, const void* h, hipStream_t st,
                          const Timing& tm = {});
-hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st, const Timing& tm = {});
+hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, int round, hipStream_t st,
+                           const Timing& tm = {});
 hipError_t launch_combine(const Layout& lo, int l, float* y, hipStream_t st, const Timing& tm = {});
 
 }  // namespace cmoe

@@ -424,11 +424,12 @@ __global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bb
 }
 
 // ---------------------------------------------------------------- fp32
-__global__ __launch_bounds__(64) void ffn_up_f32(Layout lo, int l, int bbuf, int sv, const float* __restrict__ h) {
+__global__ __launch_bounds__(64) void ffn_up_f32(Layout lo, int l, int bbuf, int sv, int round,
+                                                 const float* __restrict__ h) {
     const int ftn = lo.F / 64;
     const int e = blockIdx.x / ftn, ft = blockIdx.x - e * ftn;
     const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
-    if (m == 0) return;
+    if (m == 0 || lo.round_of[e] != round) return;
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
     const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
     if (slot < 0 || slot >= lo.n_slots) return;
@@ -461,11 +462,11 @@ __global__ __launch_bounds__(64) void ffn_up_f32(Layout lo, int l, int bbuf, int
     }
 }
 
-__global__ __launch_bounds__(64) void ffn_down_f32(Layout lo, int l, int bbuf, int sv) {
+__global__ __launch_bounds__(64) void ffn_down_f32(Layout lo, int l, int bbuf, int sv, int round) {
     const int dtn = lo.d / 64;
     const int e = blockIdx.x / dtn, dt = blockIdx.x - e * dtn;
     const int m = lo.bcount[(int64_t)bbuf * lo.N + e];
-    if (m == 0) return;
+    if (m == 0 || lo.round_of[e] != round) return;
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S;
     const int slot = lo.slot_of[((int64_t)sv * lo.L + l) * lo.N + e];
     if (slot < 0 || slot >= lo.n_slots) return;
@@ -528,7 +529,8 @@ __global__ __launch_bounds__(64) void combine_kernel(Layout lo, int l, float* __
 
 }  // namespace
 
-hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* h, hipStream_t st, const Timing& tm) {
+hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, int round, const void* h, hipStream_t st,
+                         const Timing& tm) {
     if (lo.dtype == 1) {
         const uint16_t* hb = static_cast<const uint16_t*>(h);
         if (lo.ffn_waves == kWaves)
@@ -537,13 +539,13 @@ hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, const void* 
         else
             launch_kernel(ffn_up_bf16<1>, dim3(lo.max_units * (lo.F / 16)), dim3(64), st, tm, lo, l, bbuf, sv, hb);
     } else {
-        launch_kernel(ffn_up_f32, dim3(lo.N * (lo.F / 64)), dim3(64), st, tm, lo, l, bbuf, sv,
+        launch_kernel(ffn_up_f32, dim3(lo.N * (lo.F / 64)), dim3(64), st, tm, lo, l, bbuf, sv, round,
                       static_cast<const float*>(h));
     }
     return hipGetLastError();
 }
 
-hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_t st, const Timing& tm) {
+hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, int round, hipStream_t st, const Timing& tm) {
     if (lo.dtype == 1) {
         const int dtn = lo.d / 32;
         if (lo.ffn_waves == kWaves)
@@ -552,7 +554,7 @@ hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, hipStream_
         else
             launch_kernel(ffn_down_bf16<1>, dim3(lo.max_units * dtn), dim3(64), st, tm, lo, l, bbuf, sv);
     } else {
-        launch_kernel(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), st, tm, lo, l, bbuf, sv);
+        launch_kernel(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), st, tm, lo, l, bbuf, sv, round);
     }
     return hipGetLastError();
 }

@@ -124,28 +124,37 @@ __device__ inline unsigned long long cache_word(const Layout& lo, int layer, int
 
 __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
     __shared__ unsigned long long U[4];
-    __shared__ int so[kMaxN], se[kMaxN], free_list[kMaxN], enter_list[kMaxN], lds4[4];
+    __shared__ int so[kMaxN], se[kMaxN], stp[kMaxN], rnd_s[kMaxN], free_list[kMaxN], enter_list[kMaxN],
+        victim_list[kMaxN], lds4[4];
     const int tid = threadIdx.x;
-    const int N = lo.N, layer = f.layer;
-    const int32_t* so_in = lo.slot_of + ((int64_t)f.rv * lo.L + layer) * N;
-    const int32_t* se_in = lo.slot_exp + ((int64_t)f.rv * lo.L + layer) * lo.n_slots;
+    const int N = lo.N, layer = f.layer, P = lo.n_slots;
+    const int64_t vin = (int64_t)f.rv * lo.L + layer, vout = (int64_t)(f.rv ^ 1) * lo.L + layer;
+    const int32_t* so_in = lo.slot_of + vin * N;
+    const int32_t* se_in = lo.slot_exp + vin * P;
+    const int32_t* st_in = lo.slot_stamp + vin * P;
+    const bool demand = f.kind == 0;
     // Every global load of the prologue is issued before the first is used:
-    // the slot maps, the bucket sizes for the FFN work units and the first
+    // the slot maps and stamps, the bucket sizes (the executed experts and
+    // the FFN work units), the round plan of a later round, and the first
     // batch of cache words (indices clamped; a clamped value is not used).
-    const bool units = f.bbuf >= 0 && blockIdx.x == 0;
+    const bool units = demand && f.units && blockIdx.x == 0;
     const int S_NW = lo.S * lo.NW;
     const int so_v = so_in[min(tid, N - 1)];
-    const int se_v = se_in[min(tid, lo.n_slots - 1)];
-    const int m_v = lo.bcount[(int64_t)max(f.bbuf, 0) * N + min(tid, N - 1)];
+    const int se_v = se_in[min(tid, P - 1)];
+    const int st_v = st_in[min(tid, P - 1)];
+    const int m_v = demand ? lo.bcount[(int64_t)f.bbuf * N + min(tid, N - 1)] : 0;
+    const int ro_v = (demand && f.round > 0) ? lo.round_of[min(tid, N - 1)] : -1;
     constexpr int kWords = 4;  // cache words per thread per batch
     unsigned long long w[kWords];
 #pragma unroll
     for (int u = 0; u < kWords; ++u) w[u] = cache_word(lo, layer, min(tid + u * (int)blockDim.x, S_NW - 1));
     __builtin_amdgcn_sched_barrier(0);
-    const int m_own = (units && tid < N) ? m_v : 0;
     if (tid < 4) U[tid] = 0ull;
     if (tid < N) so[tid] = so_v;
-    if (tid < lo.n_slots) se[tid] = se_v;
+    if (tid < P) {
+        se[tid] = se_v;
+        stp[tid] = st_v;
+    }
     __syncthreads();
     for (int i0 = 0; i0 < S_NW; i0 += kWords * blockDim.x) {
         if (i0 > 0) {
@@ -169,37 +178,107 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
         so[e] = -1;
         cur = -1;
     }
+    int nU = 0;
+    for (int j = 0; j < lo.NW; ++j) nU += __popcll(U[j]);
+    const bool overflow = nU > P;  // the union does not fit the arena (block-uniform)
     __syncthreads();
-    const bool enter = e < N && inU && cur < 0;
-    const bool is_free = tid < lo.n_slots && se[tid] == -1;
+    // FFN round of each expert the layer step executes.  While the union fits,
+    // all run in round 0.  Otherwise round 0 plans the rounds: the executed
+    // experts already resident first, then the others, each group ascending,
+    // P per round; later rounds read the plan.
+    const bool inE = demand && e < N && m_v > 0;
+    int rnd = -1;
+    if (demand) {
+        if (!overflow) {
+            rnd = inE ? 0 : -1;
+        } else if (f.round == 0) {
+            const bool res_e = inE && cur >= 0, mis_e = inE && cur < 0;
+            int nres, nmis;
+            const int r1 = block_scan(res_e ? 1 : 0, &nres, lds4);
+            const int r2 = block_scan(mis_e ? 1 : 0, &nmis, lds4);
+            rnd = res_e ? r1 / P : (mis_e ? (nres + r2) / P : -1);
+        } else {
+            rnd = e < N ? ro_v : -1;
+        }
+    }
+    if (e < N) rnd_s[e] = rnd;
+    const bool now = demand && rnd >= 0 && rnd == f.round;  // executed in this round
+    bool enter;
+    if (!demand) enter = e < N && inU && cur < 0;
+    else if (!overflow) enter = f.round == 0 && e < N && inU && cur < 0;
+    else enter = now && cur < 0;
+    const bool is_free = tid < P && se[tid] == -1;
     int nfree, nenter;
     const int rf = block_scan(is_free ? 1 : 0, &nfree, lds4);
     if (is_free) free_list[rf] = tid;
     const int re = block_scan(enter ? 1 : 0, &nenter, lds4);
-    __syncthreads();
-    if (enter) {  // rank re among new experts takes the rank-re free slot
-        const int q = free_list[re];
-        so[e] = q;
-        se[q] = e;
-        enter_list[re] = e;
+    // A round that needs more than the free slots evicts the least recently
+    // used experts that no remaining round needs (lower slot on ties), ranked
+    // by (stamp, slot); after refinement only free slots are filled.
+    int nvict = 0;
+    if (demand && overflow && nenter > nfree) {  // block-uniform
+        bool vict = false;
+        int rank = 0;
+        if (tid < P && se[tid] >= 0) {
+            vict = rnd_s[se[tid]] < f.round;
+            if (vict) {
+                const int sq = stp[tid];
+                for (int q2 = 0; q2 < P; ++q2) {
+                    const int v2 = se[q2];
+                    if (v2 < 0 || rnd_s[v2] >= f.round) continue;
+                    const int s2 = stp[q2];
+                    rank += (s2 < sq || (s2 == sq && q2 < tid)) ? 1 : 0;
+                }
+            }
+        }
+        if (vict) victim_list[rank] = tid;
+        nvict = __syncthreads_count(vict);
     }
+    const int nent = (!demand && overflow) ? min(nenter, nfree) : nenter;
+    __syncthreads();
+    const bool takes = enter && re < nent;
+    if (takes) {  // rank re among new experts takes the rank-re free slot, then the victims in rank order
+        int q = -1;
+        if (re < nfree)
+            q = free_list[re];
+        else if (re - nfree < nvict)
+            q = victim_list[re - nfree];
+        if (q >= 0) {
+            if (re >= nfree) so[se[q]] = -1;  // evicted
+            so[e] = q;
+            se[q] = e;
+        }
+        enter_list[re] = q >= 0 ? e : -1;  // q < 0 cannot happen: a round fits the arena
+    }
+    __syncthreads();
+    // last use: the experts executed in this round and every expert copied in
+    if (e < N && (now || takes) && so[e] >= 0) stp[so[e]] = f.clk;
     __syncthreads();
     if (blockIdx.x == 0) {
-        int32_t* so_out = lo.slot_of + ((int64_t)(f.rv ^ 1) * lo.L + layer) * N;
-        int32_t* se_out = lo.slot_exp + ((int64_t)(f.rv ^ 1) * lo.L + layer) * lo.n_slots;
+        int32_t* so_out = lo.slot_of + vout * N;
+        int32_t* se_out = lo.slot_exp + vout * P;
+        int32_t* st_out = lo.slot_stamp + vout * P;
         if (tid < N) so_out[tid] = so[tid];
-        if (tid < lo.n_slots) se_out[tid] = se[tid];
+        if (tid < P) {
+            se_out[tid] = se[tid];
+            st_out[tid] = stp[tid];
+        }
+        if (demand && f.round == 0 && tid < N) lo.round_of[tid] = rnd;
         if (tid == 0) {
-            lo.step_fills[layer * 2 + f.kind] = nenter;
+            if (demand && f.round > 0)
+                lo.step_fills[layer * 2] += nent;
+            else
+                lo.step_fills[layer * 2 + f.kind] = nent;
             if (f.zero_pre) lo.step_fills[layer * 2 + 1] = 0;
-            if (f.counted) lo.phys[layer * 2 + f.kind] += nenter;
+            if (f.counted) lo.phys[layer * 2 + f.kind] += nent;
         }
     }
-    // FFN work units of this layer step: each expert's bucket cut into passes
-    // of up to kUnitTokens tokens, each stored with its expert's new slot and
-    // its token count, so that an FFN wavefront finds all three with one load.
-    // When no bucket needs a second pass, unit e is expert e (or none if it
-    // has no tokens).
+    // FFN work units of this round: each of its experts' buckets cut into
+    // passes of up to kUnitTokens tokens, each stored with its expert's new
+    // slot and its token count, so that an FFN wavefront finds all three with
+    // one load.  When no bucket needs a second pass, unit e is expert e (or
+    // none if it has no tokens in this round).
+    const int m_own = (units && now) ? m_v : 0;
     int4* unit4 = reinterpret_cast<int4*>(lo.units);
     const bool multi = __syncthreads_or(units && m_own > kUnitTokens) != 0;
     if (units && !multi) {
@@ -240,13 +319,15 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
         }
         for (int i = total + tid; i < lo.max_units; i += blockDim.x) unit4[i] = int4{-1, -1, 0, 0};
     }
-    if (nenter == 0) return;
+    if (nent == 0) return;
     const int64_t bytes = lo.expert_elems * (lo.dtype == 1 ? 2 : 4);
     const int64_t n16 = bytes / 16;
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tid;
     const int64_t gs = (int64_t)gridDim.x * blockDim.x;
-    for (int k = 0; k < nenter; ++k) {
-        const int ex = enter_list[k], q = so[ex];
+    for (int k = 0; k < nent; ++k) {
+        const int ex = enter_list[k];
+        if (ex < 0) continue;
+        const int q = so[ex];
         const uint4* src =
             reinterpret_cast<const uint4*>(static_cast<const char*>(lo.pool) + ((int64_t)layer * N + ex) * bytes);
         uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(lo.arena) + ((int64_t)layer * lo.n_slots + q) * bytes);

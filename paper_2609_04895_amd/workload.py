@@ -14,7 +14,7 @@ def config_for(w, C: Optional[int] = None, R: Optional[int] = None, warmup_token
     """ffn_shape: None or "auto" (the library's choice), "single" or "grouped"."""
     flags = (CMOE_FLAG_FILL_ON_MAIN if fill_on_main else 0) | FFN_SHAPES[ffn_shape]
     return make_config(w.L, w.N, w.K, w.d, w.F, w.C if C is None else C, w.R if R is None else R, w.S, w.mode,
-                       w.dtype, w.pool_kind, warmup_tokens, flags, w.policy, w.lrfu_lambda)
+                       w.dtype, w.pool_kind, warmup_tokens, flags, w.policy, w.lrfu_lambda, w.arena_slots)
 
 
 def engine_for(w, inputs, C: Optional[int] = None, R: Optional[int] = None, warmup_tokens: int = 0,

@@ -82,6 +82,10 @@ def _load_hip():
                                     ctypes.c_float, ctypes.c_double, ctypes.c_int, ctypes.c_void_p,
                                     ctypes.c_void_p]
         lib.syn_dev_ar1.restype = ctypes.c_int
+        lib.syn_host_alloc.argtypes = [i64, ctypes.POINTER(ctypes.c_void_p)]
+        lib.syn_host_alloc.restype = ctypes.c_int
+        lib.syn_host_free.argtypes = [ctypes.c_void_p]
+        lib.syn_host_free.restype = ctypes.c_int
         _hip = lib
     return _hip
 
@@ -222,6 +226,36 @@ def fill_hidden_dev(w: Workload, out_ptr: int, T: Optional[int] = None, stream: 
                                    unit_scale(), int(w.dtype == DTYPE_BF16), out_ptr, stream), "hidden")
 
 
+class _PinnedBlock:
+    """hipHostMalloc memory of an exact size, freed with the last tensor that
+    views it (torch's pinned allocator rounds sizes up, which on a host that
+    limits the pinned memory of one process wastes most of that limit)."""
+
+    def __init__(self, nbytes: int):
+        p = ctypes.c_void_p()
+        rc = _load_hip().syn_host_alloc(int(nbytes), ctypes.byref(p))
+        if rc != 0 or not p.value:
+            raise MemoryError(f"hipHostMalloc of {nbytes / 1e9:.1f} GB of pinned host memory failed (hipError {rc})")
+        self.ptr = p.value
+        self.nbytes = int(nbytes)
+
+    def __del__(self):
+        if getattr(self, "ptr", None):
+            _load_hip().syn_host_free(ctypes.c_void_p(self.ptr))
+            self.ptr = None
+
+
+def pinned_host_tensor(shape, dtype):
+    """A CPU tensor over pinned, device-mapped host memory of exactly its size."""
+    import torch
+    n = int(np.prod(shape)) * torch.empty((), dtype=dtype).element_size()
+    block = _PinnedBlock(n)
+    raw = np.ctypeslib.as_array((ctypes.c_uint8 * n).from_address(block.ptr))
+    t = torch.from_numpy(raw).view(dtype).reshape(shape)
+    t._pinned_block = block   # keeps the memory alive as long as the tensor
+    return t
+
+
 def device_inputs(w: Workload, T: Optional[int] = None, with_hidden: bool = True, stream: int = 0):
     """All inputs of a workload generated on the GPU (torch tensors on cuda:0).
 
@@ -250,7 +284,7 @@ def device_inputs(w: Workload, T: Optional[int] = None, with_hidden: bool = True
     out["bias"] = None if zb is None else torch.from_numpy(zb).to(dev)
     per = 3 * w.F * w.d
     if w.pool_kind == POOL_HOST_PINNED:
-        pool = torch.empty((w.L, w.N, per), dtype=dt, pin_memory=True)
+        pool = pinned_host_tensor((w.L, w.N, per), dt)
         stage = torch.empty((1, w.N, per), dtype=dt, device=dev)
         for l in range(w.L):  # generate one layer on the device, copy it to host
             fill_pool_dev(w, stage.data_ptr(), stream, layers=(l, l + 1))

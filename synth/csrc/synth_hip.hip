@@ -112,4 +112,18 @@ int syn_dev_ar1(uint64_t seed, uint64_t tid0, uint64_t tid_s, uint64_t tid_l, in
     return (int)hipGetLastError();
 }
 
+// Pinned, device-mapped host memory of exactly `bytes` bytes (a cold pool in
+// host memory), or NULL.  Returns a hipError_t value.
+int syn_host_alloc(int64_t bytes, void** out) {
+    *out = nullptr;
+    const hipError_t e = hipHostMalloc(out, (size_t)bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        *out = nullptr;
+    }
+    return (int)e;
+}
+
+int syn_host_free(void* p) { return p ? (int)hipHostFree(p) : 0; }
+
 }  // extern "C"

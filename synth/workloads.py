@@ -56,6 +56,7 @@ class Workload:
     sweep_R: Tuple[int, ...] = ()
     policy: int = POLICY_ROUTER
     lrfu_lambda: float = 0.5
+    arena_slots: int = 0              # HBM expert slots per layer (0: min(N, S C))
 
     @property
     def elem_bytes(self) -> int:

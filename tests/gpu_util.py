@@ -98,7 +98,8 @@ def host_routers(w):
 
 
 def oracle_run(w, **kw):
-    return oracle.Run(w.L, w.N, w.K, w.C, w.R, w.S, w.mode, policy=w.policy, lrfu_lambda=w.lrfu_lambda, **kw)
+    return oracle.Run(w.L, w.N, w.K, w.C, w.R, w.S, w.mode, policy=w.policy, lrfu_lambda=w.lrfu_lambda,
+                      arena_slots=w.arena_slots, **kw)
 
 
 def rel_err(y, ref):
