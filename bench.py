@@ -69,6 +69,13 @@ def describe(w):
             + (f", {w.arena_slots} HBM expert slots per layer" if w.arena_slots else ""))
 
 
+def fills_label(w, fills):
+    if not w.has_spatio or w.R == 0:
+        return "none (no refinement)"
+    side = fills == "side" or (fills == "auto" and w.pool_kind == 1)
+    return "side stream" if side else "main stream, in the demand fill launch"
+
+
 def cpu_baseline(w, budget_s, max_procs=16):
     """The oracle on stream 0, tokens 0.. until budget_s of oracle compute in
     one process; then the same tokens replayed by one process per host core
@@ -293,7 +300,9 @@ def main():
     ap.add_argument("--streams", type=int, default=None, help="number of decode streams S (default: the workload's)")
     ap.add_argument("--arena-slots", type=int, default=None,
                     help="HBM expert slots per layer (default 0: min(N, S C), which holds the union of the caches)")
-    ap.add_argument("--fill-on-main", action="store_true", help="run fills on the main stream")
+    ap.add_argument("--fills", choices=["auto", "main", "side"], default="auto",
+                    help="where proactive fills run (auto: the library's choice, the side stream for a host pool "
+                         "and one launch with the demand fill otherwise)")
     ap.add_argument("--ffn-shape", choices=["auto", "single", "grouped"], default="auto",
                     help="bf16 FFN workgroups: one wavefront each, or four sharing big units' activations "
                          "(auto: the library's choice from the average tokens per expert)")
@@ -363,7 +372,7 @@ def main():
     t0 = time.time()
     inputs = synth.device_inputs(w, T=T_gen)
     print(f"[bench] inputs generated on the device in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
-    eng = engine_for(w, inputs, warmup_tokens=warmup, side_stream=not args.fill_on_main, ffn_shape=args.ffn_shape)
+    eng = engine_for(w, inputs, warmup_tokens=warmup, fills=args.fills, ffn_shape=args.ffn_shape)
     hidden = inputs["hidden"]
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
     main_stream = eng.main_stream
@@ -409,7 +418,7 @@ def main():
                    "capacity": w.C, "refine_budget": w.R if w.has_spatio else 0,
                    "mode": {0: "update-only", 1: "spatio-temporal", 2: "spatio-only"}[w.mode],
                    "retention": {v: k for k, v in POLICIES.items()}[w.policy], "d": w.d, "F": w.F,
-                   "fills": "main stream" if args.fill_on_main else "side stream", "ffn_shape": args.ffn_shape,
+                   "proactive_fills": fills_label(w, args.fills), "ffn_shape": args.ffn_shape,
                    "arena_slots": w.arena_slots or min(w.N, w.S * w.C)},
     }
     # algorithmic bytes of one token step: each distinct selected expert read

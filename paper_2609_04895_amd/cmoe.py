@@ -36,6 +36,7 @@ CMOE_POOL_HOST_PINNED = 1
 CMOE_FLAG_FILL_ON_MAIN = 0x1
 CMOE_FLAG_FFN_GROUPED = 0x2
 CMOE_FLAG_FFN_SINGLE = 0x4
+CMOE_FLAG_FILL_ON_SIDE = 0x8
 
 CMOE_VIEW_LOGITS = 0
 CMOE_VIEW_SELECTED = 1

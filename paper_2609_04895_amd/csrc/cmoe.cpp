@@ -109,6 +109,8 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     if ((int64_t)c->S * c->K >= (int64_t)1 << 23) return fail(CMOE_ERR_UNSUPPORTED, "S*K too large");
     if ((c->flags & CMOE_FLAG_FFN_GROUPED) && (c->flags & CMOE_FLAG_FFN_SINGLE))
         return fail(CMOE_ERR_INVALID_ARG, "CMOE_FLAG_FFN_GROUPED and CMOE_FLAG_FFN_SINGLE exclude each other");
+    if ((c->flags & CMOE_FLAG_FILL_ON_MAIN) && (c->flags & CMOE_FLAG_FILL_ON_SIDE))
+        return fail(CMOE_ERR_INVALID_ARG, "CMOE_FLAG_FILL_ON_MAIN and CMOE_FLAG_FILL_ON_SIDE exclude each other");
     // grouped FFN workgroups pay off when buckets of more than 16 tokens are
     // common: by default, from 8 tokens per expert on average
     dv->ffn_waves = (c->flags & CMOE_FLAG_FFN_GROUPED) ? 4
@@ -278,14 +280,19 @@ hipError_t timed(cmoe_handle* hd, int kid, F&& launch) {
     return launch(tm);
 }
 
-// One residency event of `layer` (or one FFN round of it) on stream st;
+// The arguments of one residency event of `layer` (or one FFN round of it);
 // advances the layer's slot-map version and arena clock.
-hipError_t fill(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, hipStream_t st, int bbuf = 0,
-                bool units = false, int round = 0) {
+FillArgs event(cmoe_handle* hd, int layer, int kind, bool counted, bool zero_pre, int bbuf = 0, bool units = false,
+               int round = 0) {
     FillArgs f{layer, kind, hd->ver[layer], counted ? 1 : 0, zero_pre ? 1 : 0, bbuf, units ? 1 : 0, round,
                ++hd->clk[layer]};
     hd->ver[layer] ^= 1;
-    return timed(hd, KID_FILL, [&](const cmoe::Timing& tm) { return cmoe::launch_fill(*hd->cur, f, st, tm); });
+    return f;
+}
+
+// One fill launch on stream st: event f, and event g of another layer if given.
+hipError_t fill(cmoe_handle* hd, const FillArgs& f, hipStream_t st, const FillArgs* g = nullptr) {
+    return timed(hd, KID_FILL, [&](const cmoe::Timing& tm) { return cmoe::launch_fill(*hd->cur, f, g, st, tm); });
 }
 
 // One decode token.  h == nullptr selects injected logits (no router, no FFN).
@@ -316,7 +323,7 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
             HIPCHK(hipEventRecord(hd->ev_access[0], M), "event record");
             HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[0], 0), "stream wait");
         }
-        HIPCHK(fill(hd, 0, 1, counted, false, Sd), "fill");
+        HIPCHK(fill(hd, event(hd, 0, 1, counted, false), Sd), "fill");
         if (!hd->side_is_main) HIPCHK(hipEventRecord(hd->ev_pro[0], Sd), "event record");
     }
     for (int l = 0; l < c.L; ++l) {
@@ -338,20 +345,25 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
         HIPCHK(timed(hd, KID_CACHE, [&](const cmoe::Timing& tm) { return cmoe::launch_cache_step(lo, a, M, tm); }),
                "cache step");
         hd->g += 1;
-        // demand loads gate this layer's FFN; the same launch lays out the FFN
+        // Demand loads gate this layer's FFN; the same launch lays out the FFN
         // work units.  An arena smaller than the union of the caches runs the
-        // FFN in rounds, each after the fill that brings its experts in.
+        // FFN in rounds, each after the fill that brings its experts in.  The
+        // proactive loads of layer l + 1 follow the same cache step: on the
+        // main stream they join the first demand launch; on the side stream
+        // they overlap this layer's FFN.
         for (int r = 0; r < hd->dv.rounds; ++r) {
-            HIPCHK(fill(hd, l, 0, counted, r == 0 && !refine_on, M, bbuf, !inject, r), "fill");
-            if (r == 0 && refine_next) {
-                if (hd->side_is_main) {
-                    HIPCHK(fill(hd, l + 1, 1, counted, false, M), "fill");
-                } else {
-                    HIPCHK(hipEventRecord(hd->ev_access[l], M), "event record");
-                    HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[l], 0), "stream wait");
-                    HIPCHK(fill(hd, l + 1, 1, counted, false, Sd), "fill");
-                    HIPCHK(hipEventRecord(hd->ev_pro[l + 1], Sd), "event record");
-                }
+            const FillArgs dem = event(hd, l, 0, counted, r == 0 && !refine_on, bbuf, !inject, r);
+            if (r == 0 && refine_next && hd->side_is_main) {
+                const FillArgs pro = event(hd, l + 1, 1, counted, false);
+                HIPCHK(fill(hd, dem, M, &pro), "fill");
+            } else {
+                HIPCHK(fill(hd, dem, M), "fill");
+            }
+            if (r == 0 && refine_next && !hd->side_is_main) {
+                HIPCHK(hipEventRecord(hd->ev_access[l], M), "event record");
+                HIPCHK(hipStreamWaitEvent(Sd, hd->ev_access[l], 0), "stream wait");
+                HIPCHK(fill(hd, event(hd, l + 1, 1, counted, false), Sd), "fill");
+                HIPCHK(hipEventRecord(hd->ev_pro[l + 1], Sd), "event record");
             }
             if (!inject) {
                 const int sv = hd->ver[l];
@@ -460,7 +472,10 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     hd->ver.assign(cfg->L, 0);
     hd->clk.assign(cfg->L, 0);
     hd->main = static_cast<hipStream_t>(main_stream);
-    hd->side_is_main = side_stream == nullptr || side_stream == main_stream || (cfg->flags & CMOE_FLAG_FILL_ON_MAIN);
+    // proactive loads run on the side stream only where they can overlap real
+    // copies: a pool in host memory (or when asked for)
+    hd->side_is_main = side_stream == nullptr || side_stream == main_stream || (cfg->flags & CMOE_FLAG_FILL_ON_MAIN) ||
+                       (cfg->pool_kind == CMOE_POOL_DEVICE && !(cfg->flags & CMOE_FLAG_FILL_ON_SIDE));
     hd->side = hd->side_is_main ? hd->main : static_cast<hipStream_t>(side_stream);
 
     Layout& lo = hd->lo;

@@ -123,7 +123,9 @@ hipError_t launch_init(const Layout& lo, hipStream_t st);  // state, and the wor
 hipError_t launch_prep_workspace(const Layout& lo, hipStream_t st);
 hipError_t launch_router(const Layout& lo, int l, const void* h, hipStream_t st, const Timing& tm = {});
 hipError_t launch_cache_step(const Layout& lo, const StepArgs& a, hipStream_t st, const Timing& tm = {});
-hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st, const Timing& tm = {});
+// g (or NULL): a second event of another layer in the same launch
+hipError_t launch_fill(const Layout& lo, const FillArgs& f, const FillArgs* g, hipStream_t st,
+                       const Timing& tm = {});
 hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, int round, const void* h, hipStream_t st,
                          const Timing& tm = {});
 hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, int round, hipStream_t st,

@@ -122,10 +122,22 @@ __device__ inline unsigned long long cache_word(const Layout& lo, int layer, int
     return lo.cache[((int64_t)s * lo.L + layer) * lo.NW + j];
 }
 
-__global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
-    __shared__ unsigned long long U[4];
-    __shared__ int so[kMaxN], se[kMaxN], stp[kMaxN], rnd_s[kMaxN], free_list[kMaxN], enter_list[kMaxN],
-        victim_list[kMaxN], lds4[4];
+// Workgroup-local state of one residency event.
+struct FillLds {
+    unsigned long long U[4];
+    int so[kMaxN], se[kMaxN], stp[kMaxN], rnd_s[kMaxN], free_list[kMaxN], enter_list[kMaxN], victim_list[kMaxN];
+    int lds4[4];
+    __align__(16) int key[kMaxN];
+    int by_rank[kMaxN], who[kMaxN], m_rank[kMaxN];
+};
+
+// One residency event (or one FFN round of one), run by nwg workgroups of the
+// launch, this one being number wg; returns once its share of the copies is
+// done.  Workgroup 0 of the event writes the new slot maps and work units.
+__device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs& f, FillLds& sm, int wg, int nwg) {
+    unsigned long long* U = sm.U;
+    int *so = sm.so, *se = sm.se, *stp = sm.stp, *rnd_s = sm.rnd_s, *free_list = sm.free_list;
+    int *enter_list = sm.enter_list, *victim_list = sm.victim_list, *lds4 = sm.lds4;
     const int tid = threadIdx.x;
     const int N = lo.N, layer = f.layer, P = lo.n_slots;
     const int64_t vin = (int64_t)f.rv * lo.L + layer, vout = (int64_t)(f.rv ^ 1) * lo.L + layer;
@@ -137,7 +149,7 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
     // the slot maps and stamps, the bucket sizes (the executed experts and
     // the FFN work units), the round plan of a later round, and the first
     // batch of cache words (indices clamped; a clamped value is not used).
-    const bool units = demand && f.units && blockIdx.x == 0;
+    const bool units = demand && f.units && wg == 0;
     const int S_NW = lo.S * lo.NW;
     const int so_v = so_in[min(tid, N - 1)];
     const int se_v = se_in[min(tid, P - 1)];
@@ -254,7 +266,7 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
     // last use: the experts executed in this round and every expert copied in
     if (e < N && (now || takes) && so[e] >= 0) stp[so[e]] = f.clk;
     __syncthreads();
-    if (blockIdx.x == 0) {
+    if (wg == 0) {
         int32_t* so_out = lo.slot_of + vout * N;
         int32_t* se_out = lo.slot_exp + vout * P;
         int32_t* st_out = lo.slot_stamp + vout * P;
@@ -289,8 +301,7 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
         // otherwise experts with more tokens go first (lower index on ties),
         // so the longest units start first.  Rank of expert e = number of
         // larger keys (m << 8) | (255 - e), all distinct.
-        __shared__ __align__(16) int key[kMaxN];
-        __shared__ int by_rank[kMaxN], who[kMaxN], m_rank[kMaxN];
+        int *key = sm.key, *by_rank = sm.by_rank, *who = sm.who, *m_rank = sm.m_rank;
         const int m = m_own;
         const int mykey = (m << 8) | (255 - tid);
         key[tid] = tid < N ? mykey : -1;  // blockDim.x == kMaxN: every entry is written
@@ -322,8 +333,8 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
     if (nent == 0) return;
     const int64_t bytes = lo.expert_elems * (lo.dtype == 1 ? 2 : 4);
     const int64_t n16 = bytes / 16;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tid;
-    const int64_t gs = (int64_t)gridDim.x * blockDim.x;
+    const int64_t gid = (int64_t)wg * blockDim.x + tid;
+    const int64_t gs = (int64_t)nwg * blockDim.x;
     for (int k = 0; k < nent; ++k) {
         const int ex = enter_list[k];
         if (ex < 0) continue;
@@ -363,10 +374,27 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f) {
     }
 }
 
+// One residency event, or two of different layers (g.layer >= 0): the
+// demand event of one layer and the proactive event of the next, which both
+// follow the same cache step, in one launch, each on half the workgroups
+// (even ones: f, odd ones: g).
+__global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f, FillArgs g) {
+    __shared__ FillLds sm;
+    if (g.layer < 0)
+        residency_event(lo, f, sm, blockIdx.x, gridDim.x);
+    else if ((blockIdx.x & 1) == 0)
+        residency_event(lo, f, sm, blockIdx.x >> 1, (gridDim.x + 1) >> 1);
+    else
+        residency_event(lo, g, sm, blockIdx.x >> 1, gridDim.x >> 1);
+}
+
 }  // namespace
 
-hipError_t launch_fill(const Layout& lo, const FillArgs& f, hipStream_t st, const Timing& tm) {
-    launch_kernel(fill_kernel, dim3(lo.pool_host ? kFillBlocksHost : kFillBlocksDevice), dim3(256), st, tm, lo, f);
+hipError_t launch_fill(const Layout& lo, const FillArgs& f, const FillArgs* g, hipStream_t st, const Timing& tm) {
+    FillArgs none{};
+    none.layer = -1;
+    launch_kernel(fill_kernel, dim3(lo.pool_host ? kFillBlocksHost : kFillBlocksDevice), dim3(256), st, tm, lo, f,
+                  g ? *g : none);
     return hipGetLastError();
 }
 

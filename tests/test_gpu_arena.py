@@ -54,7 +54,7 @@ def test_arena_cache_path_bit_exact(case):
     w = torch.zeros((L, N, d), dtype=torch.float32, device=dev)
     pool = torch.arange(L * N * 3 * d * F, dtype=torch.float32, device=dev).reshape(L, N, 3 * d * F)
     cfg = B.make_config(L, N, K, d, F, C, R, S, mode, B.CMOE_F32, B.CMOE_POOL_DEVICE, warmup,
-                        0 if side else B.CMOE_FLAG_FILL_ON_MAIN, policy, 0.5, P)
+                        B.CMOE_FLAG_FILL_ON_SIDE if side else 0, policy, 0.5, P)
     has_t = policy == P_R
     has_s = mode != M_T
     eng = B.Engine(cfg, w, w if has_t else None, w if has_s else None, None, pool,

@@ -19,7 +19,7 @@ def make_engine(L, N, K, C, R, S, mode, warmup=0, side=True, d=64, F=64):
     w = torch.zeros((L, N, d), dtype=torch.float32, device=dev)
     pool = torch.arange(L * N * 3 * d * F, dtype=torch.float32, device=dev).reshape(L, N, 3 * d * F)
     cfg = B.make_config(L, N, K, d, F, C, R, S, mode, B.CMOE_F32, B.CMOE_POOL_DEVICE, warmup,
-                        0 if side else B.CMOE_FLAG_FILL_ON_MAIN)
+                        B.CMOE_FLAG_FILL_ON_SIDE if side else 0)
     eng = B.Engine(cfg, w, w, w if mode == 1 else None, None, pool,
                    side_stream=torch.cuda.Stream() if side else None)
     return eng, pool

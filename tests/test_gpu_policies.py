@@ -33,7 +33,7 @@ def make_engine(L, N, K, C, R, S, mode, policy, lam=0.5, warmup=0, side=True, d=
     w = torch.zeros((L, N, d), dtype=torch.float32, device=dev)
     pool = torch.arange(L * N * 3 * d * F, dtype=torch.float32, device=dev).reshape(L, N, 3 * d * F)
     cfg = B.make_config(L, N, K, d, F, C, R, S, mode, B.CMOE_F32, B.CMOE_POOL_DEVICE, warmup,
-                        0 if side else B.CMOE_FLAG_FILL_ON_MAIN, policy, lam)
+                        B.CMOE_FLAG_FILL_ON_SIDE if side else 0, policy, lam)
     eng = B.Engine(cfg, w, None, w if mode == SPATIO_ONLY else None, None, pool,
                    side_stream=torch.cuda.Stream() if side else None)
     return eng

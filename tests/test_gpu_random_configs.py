@@ -67,7 +67,7 @@ def test_random_config_cache_path_bit_exact(case):
     w = torch.zeros((L, N, d), dtype=torch.float32, device=dev)
     pool = torch.arange(L * N * 3 * d * F, dtype=torch.float32, device=dev).reshape(L, N, 3 * d * F)
     cfg = B.make_config(L, N, K, d, F, C, R, S, mode, B.CMOE_F32, B.CMOE_POOL_DEVICE, c["warmup"],
-                        0 if c["side"] else B.CMOE_FLAG_FILL_ON_MAIN, policy, c["lam"])
+                        B.CMOE_FLAG_FILL_ON_SIDE if c["side"] else 0, policy, c["lam"])
     has_t = policy == oracle.POLICY_ROUTER
     has_s = mode != oracle.MODE_TEMPORAL
     eng = B.Engine(cfg, w, w if has_t else None, w if has_s else None, None, pool,
