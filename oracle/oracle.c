@@ -163,14 +163,21 @@ void orc_topk(const float* v, int n, int k, int32_t* out) {
     }
 }
 
-/* Lowest-scoring member (allowed[u] != 0); ties: lowest index. -1 if none. */
-static int orc_argmin(const float* s, const uint8_t* allowed, int n) {
-    int best = -1;
-    for (int u = 0; u < n; ++u) {
-        if (!allowed[u]) continue;
-        if (best < 0 || s[u] < s[best]) best = u;
+/* The (up to) k members of `allowed` with the lowest scores, lowest first;
+ * equal scores: lower index first.  Returns how many there are. */
+static int orc_lowest(const float* s, const uint8_t* allowed, int n, int k, int32_t* out) {
+    uint8_t taken[ORC_NMAX];
+    memset(taken, 0, (size_t)n);
+    int found = 0;
+    while (found < k) {
+        int best = -1;
+        for (int u = 0; u < n; ++u)
+            if (allowed[u] && !taken[u] && (best < 0 || s[u] < s[best])) best = u;
+        if (best < 0) break;
+        taken[best] = 1;
+        out[found++] = best;
     }
-    return best;
+    return found;
 }
 
 static int orc_count(const uint8_t* c, int n) {
@@ -180,69 +187,76 @@ static int orc_count(const uint8_t* c, int n) {
 }
 
 /* ------------------------------------------------------------------ */
-/* Algorithm 1: shared post-access cache update U_B(C, S, s)           */
+/* Post-access retention U_B(C, S, s) (Section 3.2, Algorithm 1)        */
 /* ------------------------------------------------------------------ */
-/* C: membership [N] (0/1), updated in place.  S: the K selected experts.
- * s: retention priority (s^T).  demand (may be NULL): receives S \ C in
- * ascending order.  Returns |S \ C|. */
+/* After the access every selected expert is resident: the demand misses
+ * D = S \ C are loaded, and nothing else is admitted.  When C u S exceeds
+ * the capacity, the surplus leaves: the residents outside S with the lowest
+ * priority, lower index first among equal priorities (the residents that
+ * Algorithm 1 evicts one demand at a time, since S is protected and the
+ * candidates for eviction only shrink).
+ * C: membership [N] (0/1), updated in place.  S: the K selected experts.
+ * s: retention priority (s^T).  demand (may be NULL): receives D in
+ * ascending order.  Returns |D|. */
 int orc_update_cache(uint8_t* C, int N, int cap, const int32_t* S, int K, const float* s,
                      int32_t* demand) {
-    uint8_t sel[ORC_NMAX];
+    uint8_t sel[ORC_NMAX], leavable[ORC_NMAX];
     memset(sel, 0, (size_t)N);
     for (int k = 0; k < K; ++k) sel[S[k]] = 1;
     int32_t D[ORC_NMAX];
     int nD = 0;
     for (int e = 0; e < N; ++e)
-        if (sel[e] && !C[e]) D[nD++] = e;     /* demand-loaded selected experts */
-    int size = orc_count(C, N);
-    for (int i = 0; i < nD; ++i) {
-        int e = D[i];
-        if (size < cap) {
-            C[e] = 1;
-            ++size;
-        } else {
-            uint8_t victims[ORC_NMAX];        /* residents not selected now */
-            for (int u = 0; u < N; ++u) victims[u] = (uint8_t)(C[u] && !sel[u]);
-            int v = orc_argmin(s, victims, N);
-            C[v] = 0;
-            C[e] = 1;
-        }
+        if (sel[e] && !C[e]) D[nD++] = e;
+    const int surplus = orc_count(C, N) + nD - cap;
+    if (surplus > 0) {
+        for (int u = 0; u < N; ++u) leavable[u] = (uint8_t)(C[u] && !sel[u]);
+        int32_t out[ORC_NMAX];
+        const int n = orc_lowest(s, leavable, N, surplus, out);
+        for (int i = 0; i < n; ++i) C[out[i]] = 0;
     }
+    for (int i = 0; i < nD; ++i) C[D[i]] = 1;
     if (demand)
         for (int i = 0; i < nD; ++i) demand[i] = D[i];
     return nD;
 }
 
 /* ------------------------------------------------------------------ */
-/* Algorithm 2 refinement: examine Top_R(s^ST) in descending order     */
+/* Pre-access refinement (Section 3.3, Algorithm 2)                     */
 /* ------------------------------------------------------------------ */
-/* C updated in place; loaded (may be NULL) receives the proactively loaded
- * experts in the order they were inserted.  Returns their number. */
+/* The candidates A = Top_R(s^ST) are examined from the highest score down.
+ * A candidate already resident stays; one that is not is loaded while the
+ * cache has room, and after that displaces the weakest resident only when
+ * its score is strictly higher.  Candidates come in non-increasing score and
+ * the weakest remaining resident never gets weaker, so the displaced experts
+ * are the weakest residents in order (lower index first among equals), and
+ * the displacements stop at the first candidate that does not beat the next
+ * of them.
+ * C updated in place; loaded (may be NULL) receives the proactively loaded
+ * experts in the order they are examined.  Returns their number. */
 int orc_refine(uint8_t* C, int N, int cap, const float* sST, int R, int32_t* loaded) {
-    int32_t A[ORC_NMAX];
+    int32_t A[ORC_NMAX], fresh[ORC_NMAX], weakest[ORC_NMAX];
     if (R > N) R = N;
     orc_topk(sST, N, R, A);
-    int size = orc_count(C, N);
-    int nP = 0;
-    for (int i = 0; i < R; ++i) {
-        int e = A[i];
-        if (C[e]) continue;
-        if (size < cap) {
-            C[e] = 1;
-            ++size;
-            if (loaded) loaded[nP] = e;
-            ++nP;
-        } else {
-            int v = orc_argmin(sST, C, N);
-            if (sST[e] > sST[v]) {
-                C[v] = 0;
-                C[e] = 1;
-                if (loaded) loaded[nP] = e;
-                ++nP;
-            }
+    int nfresh = 0;
+    for (int i = 0; i < R; ++i)
+        if (!C[A[i]]) fresh[nfresh++] = A[i];
+    const int room = cap - orc_count(C, N);
+    const int nfill = nfresh < room ? nfresh : room;
+    for (int i = 0; i < nfill; ++i) C[fresh[i]] = 1;
+    const int32_t* rest = fresh + nfill;
+    const int nrest = nfresh - nfill;
+    int nrep = 0;
+    if (nrest > 0) {
+        const int nw = orc_lowest(sST, C, N, nrest, weakest);
+        while (nrep < nrest && nrep < nw && sST[rest[nrep]] > sST[weakest[nrep]]) ++nrep;
+        for (int i = 0; i < nrep; ++i) {
+            C[weakest[i]] = 0;
+            C[rest[i]] = 1;
         }
     }
-    return nP;
+    if (loaded)
+        for (int i = 0; i < nfill + nrep; ++i) loaded[i] = fresh[i];
+    return nfill + nrep;
 }
 
 /* ------------------------------------------------------------------ */

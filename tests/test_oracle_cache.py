@@ -183,3 +183,72 @@ def test_refine_budget_zero_is_a_no_op():
     s = np.arange(6, dtype=np.float32)
     new, loaded = oracle.refine(mask(6, {0, 1}), s, 0, 3)
     assert members(new) == {0, 1} and len(loaded) == 0
+
+
+# ------------------------------------------------------------ stepwise readings
+def stepwise_update(C, S, s, cap):
+    """Algorithm 1 read step by step: each demand-loaded expert (ascending) is
+    inserted; when the cache is full the lowest-priority resident outside S
+    leaves first (lower index on ties)."""
+    C = set(C)
+    for e in sorted(set(S) - C):
+        if len(C) >= cap:
+            v = min(C - set(S), key=lambda u: (s[u], u))
+            C.remove(v)
+        C.add(e)
+    return C
+
+
+def stepwise_refine(C, s, R, cap):
+    """The refinement loop read step by step: candidates Top_R(s) from the
+    highest score (lower index first on ties); a non-resident one enters while
+    there is room, else replaces the weakest resident (lower index on ties)
+    only if strictly higher.  Returns (cache, loaded in order)."""
+    C = set(C)
+    loaded = []
+    for e in sorted(range(len(s)), key=lambda u: (-s[u], u))[:R]:
+        if e in C:
+            continue
+        if len(C) < cap:
+            C.add(e)
+            loaded.append(e)
+        else:
+            v = min(C, key=lambda u: (s[u], u))
+            if s[e] > s[v]:
+                C.remove(v)
+                C.add(e)
+                loaded.append(e)
+    return C, loaded
+
+
+@pytest.mark.parametrize("N", [4, 5, 6])
+def test_update_cache_equals_the_stepwise_reading_with_ties(N):
+    rng = np.random.default_rng(100 + N)
+    score_sets = [rng.integers(0, 3, N).astype(np.float32) for _ in range(8)]
+    for cap in range(1, N + 1):
+        for K in range(1, cap + 1):
+            for csize in range(0, cap + 1):
+                for C in subsets(range(N), csize):
+                    for S in subsets(range(N), K):
+                        for s in score_sets:
+                            got = members(oracle.update_cache(mask(N, C), sorted(S), s, cap)[0])
+                            assert got == stepwise_update(C, S, s, cap)
+
+
+@pytest.mark.parametrize("N", [4, 5, 6, 7])
+def test_refine_equals_the_stepwise_reading_with_ties(N):
+    rng = np.random.default_rng(200 + N)
+    score_sets = [rng.integers(0, 3, N).astype(np.float32) for _ in range(6)]
+    score_sets += [rng.random(N).astype(np.float32) for _ in range(2)]
+    n = 0
+    for cap in range(1, N + 1):
+        for csize in range(0, cap + 1):
+            for C in subsets(range(N), csize):
+                for R in range(0, N + 1):
+                    for s in score_sets:
+                        new, loaded = oracle.refine(mask(N, C), s, R, cap)
+                        want, want_loaded = stepwise_refine(C, s, R, cap)
+                        assert members(new) == want
+                        assert loaded.tolist() == want_loaded
+                        n += 1
+    assert n > 1000

@@ -22,12 +22,13 @@ ARENA = ["tests/test_oracle_arena.py"]
 
 # (name, source text, replacement, pins expected to catch it)
 MISTAKES = [
-    ("refinement replaces on equal score", "if (sST[e] > sST[v]) {", "if (sST[e] >= sST[v]) {", CACHE),
-    ("argmin evicts the higher index on ties", "if (best < 0 || s[u] < s[best]) best = u;",
-     "if (best < 0 || s[u] <= s[best]) best = u;", CACHE),
+    ("refinement replaces on equal score", "sST[rest[nrep]] > sST[weakest[nrep]]",
+     "sST[rest[nrep]] >= sST[weakest[nrep]]", CACHE),
+    ("lowest-priority ranking takes the higher index on ties", "(best < 0 || s[u] < s[best])) best = u;",
+     "(best < 0 || s[u] <= s[best])) best = u;", CACHE),
     ("refinement score drops p^S", "sST[e] = aT[e] + pred[e];", "sST[e] = aT[e];", CACHE),
     ("retention score drops p^R", "sT[e] = pR[e] + pT[e];", "sT[e] = pT[e];", CACHE),
-    ("selected experts not protected", "victims[u] = (uint8_t)(C[u] && !sel[u]);", "victims[u] = C[u];", CACHE),
+    ("selected experts not protected", "leavable[u] = (uint8_t)(C[u] && !sel[u]);", "leavable[u] = C[u];", CACHE),
     ("refinement at the first token", "if (spatio && t >= 1 && c->R > 0) {", "if (spatio && t >= 0 && c->R > 0) {",
      CACHE),
     ("silu sign", "act[f] = a / (1.0 + exp(-a)) * b;", "act[f] = a / (1.0 + exp(a)) * b;", PRIM),
@@ -60,8 +61,12 @@ MISTAKES = [
      "for (int i = 0; i < d; ++i) acc = (float)(acc + (double)w[i] * (double)h[i]);", PRIM),
     ("gates not renormalised", "out->gate[sl * K + k] = (double)pR[sel[k]] / gsum;",
      "out->gate[sl * K + k] = (double)pR[sel[k]];", GATES),
-    ("refinement examines candidates from the lowest score up", "        int e = A[i];\n        if (C[e]) continue;",
-     "        int e = A[R - 1 - i];\n        if (C[e]) continue;", CACHE),
+    ("refinement examines candidates from the lowest score up", "if (!C[A[i]]) fresh[nfresh++] = A[i];",
+     "if (!C[A[R - 1 - i]]) fresh[nfresh++] = A[R - 1 - i];", CACHE),
+    ("refinement displaces without checking the next weakest", "while (nrep < nrest && nrep < nw && ",
+     "while (nrep < nrest && nrep < nw && nrep < 1 && ", CACHE),
+    ("retention evicts one too few", "const int surplus = orc_count(C, N) + nD - cap;",
+     "const int surplus = orc_count(C, N) + nD - cap - 1;", CACHE),
     ("down projection transposed", "acc += (double)wd[(size_t)j * F + f] * act[f];",
      "acc += (double)wd[(size_t)f * d + j] * act[f];", PRIM),
     ("up projection reads the gate weights", "b += (double)wu[(size_t)f * d + i] * (double)x[i];",
