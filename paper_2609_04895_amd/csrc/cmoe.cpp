@@ -506,6 +506,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.slot_stamp = reinterpret_cast<int32_t*>(sb + p.slot_stamp);
     lo.max_units = max_units(cfg);
     lo.ffn_waves = dv.ffn_waves;
+    lo.unit_tokens = dv.ffn_waves > 1 ? cmoe::kUnitTokensGrouped : cmoe::kUnitTokens;
     hd->lo_static = lo;
     bind_workspace(lo, static_cast<char*>(buf->workspace), p);
     bind_workspace(hd->lo_static, hd->scratch_fits ? static_cast<char*>(scratch_dev) : nullptr, p);

@@ -19,13 +19,17 @@ constexpr int kStreamsPerBlock = 1;   // cache-step kernel: one wavefront per st
 // flight (512 workgroups copy 2.7 times faster than 128); reads over the
 // host link peak with fewer (128: 56 GB/s, 1024: 47 GB/s)
 constexpr int kFillBlocksDevice = 512, kFillBlocksHost = 128;
-constexpr int kUnitTokens = 64;   // FFN work unit: up to 64 tokens of one expert (one pass over its weights)
+// FFN work unit: one pass over an expert's weights for up to this many of its
+// tokens: 64 with one wavefront per workgroup, 128 in the grouped launch
+// (whose workgroups stage the activations in LDS for the four row tiles)
+constexpr int kUnitTokens = 64, kUnitTokensGrouped = 128;
 
 // Every pointer the kernels use, carved out of the caller's buffers.
 struct Layout {
     int32_t L, N, K, d, F, C, S, mode, dtype, NW, n_slots, n_r, nsplit, rdk, zstride, warmup;
     int32_t iT, iS;        // router slot of the Temporal / Spatio Router, -1 if not used
     int32_t max_units;     // FFN work units per layer step, at most N + ceil(S K / kUnitTokens)
+    int32_t unit_tokens;   // tokens per work unit: kUnitTokens, or kUnitTokensGrouped (grouped launch)
     int32_t ffn_waves;     // wavefronts per bf16 FFN workgroup: 1, or 4 (grouped: units of more
                            // than 16 tokens share their activations through LDS)
     int32_t policy;        // retention priority (cmoe_policy)

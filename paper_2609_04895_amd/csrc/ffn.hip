@@ -45,6 +45,8 @@ constexpr int kUnrollSolo = 1;  // k chunks per load block, kNG token groups in 
                                 // path is rare in the launches that use it, and a deeper block would
                                 // set the register budget (and so the occupancy) of the whole kernel
 constexpr int kWaves = 4;       // wavefronts per grouped workgroup: consecutive row tiles of one work unit
+constexpr int kNGWide = kUnitTokensGrouped / 16;  // token groups of the widest pass (grouped launch)
+static_assert(kNGWide == 8, "the wide staging split gives each thread four of the eight groups");
 
 __device__ inline bf16x8 as_bf16x8(uint4 v) {
     bf16x8 r;
@@ -233,6 +235,76 @@ __device__ inline void mfma_pass_shared(const uint4* __restrict__ tile, int nchu
     }
 }
 
+// Grouped launch, units of 65 to kUnitTokensGrouped tokens (a hot expert's
+// tokens in one pass, so its weights are streamed once): the activations of
+// one k chunk for all eight token groups (16 KB) are staged in LDS once per
+// workgroup, two buffers, one barrier per chunk.  Slot (group q, half hh)
+// holds, for lane (r, g), token column r's 8 values at k = 64 c + 32 hh + 8 g.
+// Its 32 KB share the workgroup's LDS with HeavyLds.
+struct WideLds {
+    uint4 x[2][kNGWide * 2][64];
+};
+union GroupedLds {
+    HeavyLds<kUnrollWide> narrow;
+    WideLds wide;
+};
+
+// Staging of thread tid: groups 4 (tid / 128) .. + 3 at half (tid / 64) % 2
+// of chunk c (clamped; a chunk past the end is never used), from the token
+// rows xs of those four groups.
+__device__ __forceinline__ Staged wide_stage_load(const uint16_t* const* xs, int c, int nchunk, int tid) {
+    const int off = min(c, nchunk - 1) * 64 + 32 * ((tid >> 6) & 1);
+    Staged st;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) st.v[q] = *reinterpret_cast<const uint4*>(xs[q] + off);
+    return st;
+}
+
+__device__ __forceinline__ void wide_stage_store(uint4 (*xb)[64], int tid, int ng, const Staged& st) {
+    const int q0 = 4 * (tid >> 7), hh = (tid >> 6) & 1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        if (q0 + q < ng) xb[(q0 + q) * 2 + hh][tid & 63] = st.v[q];
+}
+
+// One pass of ng (up to 8) token groups over a 16-row (gate/up) or 2 x 16-row
+// (down) weight tile, the activations shared through LDS, one k chunk per
+// block: the next chunk's weights are loaded while the current one computes.
+// As in the four-group pass, every wavefront runs the loop and its barriers
+// and every global load is unconditional; only `active` wavefronts compute.
+__device__ __forceinline__ void mfma_pass_wide(const uint4* __restrict__ tile, int nchunk, const uint16_t* const* xs, int ng,
+                                      bool active, WideLds& sm, int tid, f32x4* acc0, f32x4* acc1) {
+    const int lane = tid & 63;
+    ng = __builtin_amdgcn_readfirstlane(ng);
+#pragma unroll
+    for (int q = 0; q < kNGWide; ++q) {
+        acc0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    Staged st = wide_stage_load(xs, 0, nchunk, tid);
+    int b = 0;
+    for (int c = 0; c < nchunk; ++c, b ^= 1) {
+        uint4 A[4];
+        const uint4* ch = tile + (int64_t)(active ? c : 0) * 256;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) A[j] = load_stream(ch + 64 * j);
+        wide_stage_store(sm.x[b], tid, ng, st);
+        __syncthreads();
+        st = wide_stage_load(xs, c + 1, nchunk, tid);
+        if (active) {
+#pragma unroll
+            for (int q = 0; q < kNGWide; ++q) {
+                if (q >= ng) break;
+                const uint4 X0 = sm.x[b][q * 2][lane], X1 = sm.x[b][q * 2 + 1][lane];
+                acc0[q] = mfma_bf16(A[0], X0, acc0[q]);
+                acc0[q] = mfma_bf16(A[1], X1, acc0[q]);
+                acc1[q] = mfma_bf16(A[2], X0, acc1[q]);
+                acc1[q] = mfma_bf16(A[3], X1, acc1[q]);
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- bf16
 // Token groups of one pass over the weights: one group (up to 16 tokens, the
 // common case) with a deep k block, or kNG groups with a shallower one.
@@ -269,8 +341,8 @@ __device__ inline void up_passes(const Layout& lo, int l, int ft, const int32_t*
     }
 }
 
-// A unit of 17 to kUnitTokens tokens: one pass with the activations shared
-// by the workgroup.
+// A unit of 17 to 16 kNG tokens: one pass with the activations shared by the
+// workgroup.
 __device__ inline void up_heavy(const Layout& lo, int l, int ft, const int32_t* __restrict__ bk, int m,
                                 const uint4* __restrict__ tileA, const uint16_t* __restrict__ h, int tid,
                                 HeavyLds<kUnrollWide>& sm) {
@@ -299,13 +371,43 @@ __device__ inline void up_heavy(const Layout& lo, int l, int ft, const int32_t* 
     }
 }
 
+// A unit of 65 to kUnitTokensGrouped tokens: one pass, eight token groups,
+// the activations shared by the workgroup.
+__device__ __forceinline__ void up_heavy_wide(const Layout& lo, int l, int ft, const int32_t* __restrict__ bk, int m,
+                                     const uint4* __restrict__ tileA, const uint16_t* __restrict__ h, int tid,
+                                     WideLds& sm) {
+    const int lane = tid & 63, r = lane & 15, g = lane >> 4;
+    const int d = lo.d, q0 = 4 * (tid >> 7);
+    uint16_t* act = reinterpret_cast<uint16_t*>(lo.act);
+    const uint16_t* xs[4];  // token rows of this thread's staging groups
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int p = bk[min(16 * (q0 + q) + r, m - 1)];
+        xs[q] = h + ((int64_t)(p >> 8) * lo.L + l) * d + 8 * g;
+    }
+    f32x4 cg[kNGWide], cu[kNGWide];
+    mfma_pass_wide(tileA, d / 64, xs, (m + 15) / 16, true, sm, tid, cg, cu);
+#pragma unroll
+    for (int q = 0; q < kNGWide; ++q) {
+        const int tok = 16 * q + r;
+        if (tok < m) {
+            uint2 o;
+            o.x = pack_bf16x2(silu_mul(cg[q][0], cu[q][0]), silu_mul(cg[q][1], cu[q][1]));
+            o.y = pack_bf16x2(silu_mul(cg[q][2], cu[q][2]), silu_mul(cg[q][3], cu[q][3]));
+            const int pair = bk[tok];
+            const int64_t row = (int64_t)(pair >> 8) * lo.K + (pair & 255);
+            *reinterpret_cast<uint2*>(act + row * lo.F + ft * 16 + 4 * g) = o;
+        }
+    }
+}
+
 // Work unit u (the fill kernel lays them out, heaviest first) = tokens
-// [kUnitTokens p, kUnitTokens (p + 1)) of expert e's bucket; workgroup
+// [ut p, ut (p + 1)) of expert e's bucket, ut = lo.unit_tokens; workgroup
 // (u, j) runs that pass for the W 16-row F-tiles W j + wavefront (F is a
 // multiple of 64, so every wavefront has a tile).  W = 1: every wavefront
 // on its own; W = kWaves: grouped.
 template <int W>
-__global__ __launch_bounds__(64 * W) void ffn_up_bf16(Layout lo, int l, int bbuf, int /*sv: slots come with the units*/,
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(3))) void ffn_up_bf16(Layout lo, int l, int bbuf, int /*sv: slots come with the units*/,
                                                       const uint16_t* __restrict__ h) {
     const int wgn = lo.F / (16 * W);
     const int u = blockIdx.x / wgn;
@@ -313,7 +415,7 @@ __global__ __launch_bounds__(64 * W) void ffn_up_bf16(Layout lo, int l, int bbuf
     const int ft = (blockIdx.x - u * wgn) * W + (threadIdx.x >> 6);
     const int4 ui = reinterpret_cast<const int4*>(lo.units)[u];  // expert, pass, slot, tokens in one load
     if (ui.x < 0) return;
-    const int e = ui.x & 255, t0 = kUnitTokens * (ui.x >> 8), slot = ui.y, m = ui.z;
+    const int e = ui.x & 255, t0 = lo.unit_tokens * (ui.x >> 8), slot = ui.y, m = ui.z;
     if (m <= 0 || slot < 0 || slot >= lo.n_slots) return;
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S + t0;
     // packed slot layout: chunk c of this row tile is 256 units of 16 bytes,
@@ -325,8 +427,11 @@ __global__ __launch_bounds__(64 * W) void ffn_up_bf16(Layout lo, int l, int bbuf
     } else if constexpr (W == 1) {
         up_passes<kNG, kUnrollSolo>(lo, l, ft, bk, m, tileA, h, lane);
     } else {
-        __shared__ HeavyLds<kUnrollWide> sm;
-        up_heavy(lo, l, ft, bk, m, tileA, h, threadIdx.x, sm);
+        __shared__ GroupedLds sm;
+        if (m <= 16 * kNG)
+            up_heavy(lo, l, ft, bk, m, tileA, h, threadIdx.x, sm.narrow);
+        else
+            up_heavy_wide(lo, l, ft, bk, m, tileA, h, threadIdx.x, sm.wide);
     }
 }
 
@@ -362,7 +467,7 @@ __device__ inline void down_passes(const Layout& lo, int l, int dt, const int32_
     }
 }
 
-// A unit of 17 to kUnitTokens tokens in the grouped launch: one pass with
+// A unit of 17 to 16 kNG tokens in the grouped launch: one pass with
 // the SwiGLU intermediate shared by the workgroup.  Wavefronts past the last
 // d-tile (d not a multiple of 32 W) take part in the staging and barriers
 // only.
@@ -394,9 +499,40 @@ __device__ inline void down_heavy(const Layout& lo, int l, int dt, bool active, 
     }
 }
 
+// A unit of 65 to kUnitTokensGrouped tokens in the grouped launch: one pass,
+// eight token groups, the SwiGLU intermediate shared by the workgroup.
+__device__ __forceinline__ void down_heavy_wide(const Layout& lo, int l, int dt, bool active, const int32_t* __restrict__ bk,
+                                       int m, const uint4* __restrict__ tileB, int tid, WideLds& sm) {
+    const int lane = tid & 63, r = lane & 15, g = lane >> 4;
+    const int F = lo.F, q0 = 4 * (tid >> 7);
+    const uint16_t* act = reinterpret_cast<const uint16_t*>(lo.act);
+    const uint16_t* xs[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int p = bk[min(16 * (q0 + q) + r, m - 1)];
+        xs[q] = act + ((int64_t)(p >> 8) * lo.K + (p & 255)) * F + 8 * g;
+    }
+    f32x4 c0[kNGWide], c1[kNGWide];
+    mfma_pass_wide(tileB, F / 64, xs, (m + 15) / 16, active, sm, tid, c0, c1);
+    if (!active) return;
+#pragma unroll
+    for (int q = 0; q < kNGWide; ++q) {
+        const int tok = 16 * q + r;
+        if (tok < m) {
+            const int pair = bk[tok];
+            const int s = pair >> 8, k = pair & 255;
+            const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
+            float* dst = lo.yp + ((int64_t)s * lo.K + k) * lo.d + dt * 32 + 4 * g;
+            *reinterpret_cast<float4*>(dst) = make_float4(gk * c0[q][0], gk * c0[q][1], gk * c0[q][2], gk * c0[q][3]);
+            *reinterpret_cast<float4*>(dst + 16) =
+                make_float4(gk * c1[q][0], gk * c1[q][1], gk * c1[q][2], gk * c1[q][3]);
+        }
+    }
+}
+
 // Workgroup (u, j): the W 32-row d-tiles W j + wavefront of unit u.
 template <int W>
-__global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bbuf, int /*sv: slots come with the units*/) {
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(3))) void ffn_down_bf16(Layout lo, int l, int bbuf, int /*sv: slots come with the units*/) {
     const int dtn = lo.d / 32;
     const int wgn = (dtn + W - 1) / W;
     const int u = blockIdx.x / wgn;
@@ -405,7 +541,7 @@ __global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bb
     const bool active = dt < dtn;
     const int4 ui = reinterpret_cast<const int4*>(lo.units)[u];  // expert, pass, slot, tokens in one load
     if (ui.x < 0) return;
-    const int e = ui.x & 255, t0 = kUnitTokens * (ui.x >> 8), slot = ui.y, m = ui.z;
+    const int e = ui.x & 255, t0 = lo.unit_tokens * (ui.x >> 8), slot = ui.y, m = ui.z;
     if (m <= 0 || slot < 0 || slot >= lo.n_slots) return;
     const int32_t* bk = lo.pairs + ((int64_t)bbuf * lo.N + e) * lo.S + t0;
     // packed slot layout: after the gate/up part (F d / 4 units), chunk c of
@@ -418,8 +554,11 @@ __global__ __launch_bounds__(64 * W) void ffn_down_bf16(Layout lo, int l, int bb
     } else if constexpr (W == 1) {
         down_passes<kNG, kUnrollSolo>(lo, l, dt, bk, m, tileB, lane);
     } else {
-        __shared__ HeavyLds<kUnrollWide> sm;
-        down_heavy(lo, l, dt, active, bk, m, tileB, threadIdx.x, sm);
+        __shared__ GroupedLds sm;
+        if (m <= 16 * kNG)
+            down_heavy(lo, l, dt, active, bk, m, tileB, threadIdx.x, sm.narrow);
+        else
+            down_heavy_wide(lo, l, dt, active, bk, m, tileB, threadIdx.x, sm.wide);
     }
 }
 

@@ -286,13 +286,14 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         }
     }
     // FFN work units of this round: each of its experts' buckets cut into
-    // passes of up to kUnitTokens tokens, each stored with its expert's new
+    // passes of up to lo.unit_tokens tokens, each stored with its expert's new
     // slot and its token count, so that an FFN wavefront finds all three with
     // one load.  When no bucket needs a second pass, unit e is expert e (or
     // none if it has no tokens in this round).
     const int m_own = (units && now) ? m_v : 0;
     int4* unit4 = reinterpret_cast<int4*>(lo.units);
-    const bool multi = __syncthreads_or(units && m_own > kUnitTokens) != 0;
+    const int ut = lo.unit_tokens;
+    const bool multi = __syncthreads_or(units && m_own > ut) != 0;
     if (units && !multi) {
         // blockDim.x >= N: thread e holds expert e's bucket size
         for (int i = tid; i < lo.max_units; i += blockDim.x)
@@ -315,7 +316,7 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
             }
         }
         if (tid < N) {
-            by_rank[rank] = (m + kUnitTokens - 1) / kUnitTokens;
+            by_rank[rank] = (m + ut - 1) / ut;
             who[rank] = tid;
             m_rank[rank] = m;
         }
@@ -326,7 +327,7 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         if (tid < N) {
             const int e = who[tid];
             for (int q = 0; q < passes; ++q)
-                unit4[off + q] = int4{(q << 8) | e, so[e], min(kUnitTokens, m_rank[tid] - kUnitTokens * q), 0};
+                unit4[off + q] = int4{(q << 8) | e, so[e], min(ut, m_rank[tid] - ut * q), 0};
         }
         for (int i = total + tid; i < lo.max_units; i += blockDim.x) unit4[i] = int4{-1, -1, 0, 0};
     }
