@@ -77,6 +77,21 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
     return (a >> 16) | (b & 0xFFFF0000u);
 }
 
+// The FFN grids hold wgn workgroups per work unit.  Workgroup b takes unit
+// u = 8 (q / wgn) + b % 8 and part q % wgn of it, q = b / 8, so that all the
+// workgroups of a unit have the same b % 8.  Consecutive workgroups go to the
+// eight XCDs in turn, so a unit runs on one XCD and its tokens' activations
+// are fetched into one L2 instead of eight.  Units come heaviest first, and
+// each XCD takes every eighth one.  The grid is rounded up to whole groups
+// of eight units; u may exceed the last unit.
+__device__ inline void unit_of_block(int b, int wgn, int& u, int& j) {
+    const int q = b >> 3, g = q / wgn;
+    u = g * 8 + (b & 7);
+    j = q - g * wgn;
+}
+
+inline int unit_groups(const Layout& lo) { return (lo.max_units + 7) / 8 * 8; }
+
 __device__ inline const uint16_t* slot_base(const Layout& lo, int l, int slot) {
     return reinterpret_cast<const uint16_t*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems;
 }
@@ -410,9 +425,11 @@ template <int W>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(3))) void ffn_up_bf16(Layout lo, int l, int bbuf, int /*sv: slots come with the units*/,
                                                       const uint16_t* __restrict__ h) {
     const int wgn = lo.F / (16 * W);
-    const int u = blockIdx.x / wgn;
+    int u, j;
+    unit_of_block(blockIdx.x, wgn, u, j);
+    if (u >= lo.max_units) return;
     const int lane = threadIdx.x & 63;
-    const int ft = (blockIdx.x - u * wgn) * W + (threadIdx.x >> 6);
+    const int ft = j * W + (threadIdx.x >> 6);
     const int4 ui = reinterpret_cast<const int4*>(lo.units)[u];  // expert, pass, slot, tokens in one load
     if (ui.x < 0) return;
     const int e = ui.x & 255, t0 = lo.unit_tokens * (ui.x >> 8), slot = ui.y, m = ui.z;
@@ -535,9 +552,11 @@ template <int W>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(3))) void ffn_down_bf16(Layout lo, int l, int bbuf, int /*sv: slots come with the units*/) {
     const int dtn = lo.d / 32;
     const int wgn = (dtn + W - 1) / W;
-    const int u = blockIdx.x / wgn;
+    int u, j;
+    unit_of_block(blockIdx.x, wgn, u, j);
+    if (u >= lo.max_units) return;
     const int lane = threadIdx.x & 63;
-    const int dt = (blockIdx.x - u * wgn) * W + (threadIdx.x >> 6);
+    const int dt = j * W + (threadIdx.x >> 6);
     const bool active = dt < dtn;
     const int4 ui = reinterpret_cast<const int4*>(lo.units)[u];  // expert, pass, slot, tokens in one load
     if (ui.x < 0) return;
@@ -673,10 +692,10 @@ hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, int round, c
     if (lo.dtype == 1) {
         const uint16_t* hb = static_cast<const uint16_t*>(h);
         if (lo.ffn_waves == kWaves)
-            launch_kernel(ffn_up_bf16<kWaves>, dim3(lo.max_units * (lo.F / (16 * kWaves))), dim3(64 * kWaves), st, tm,
+            launch_kernel(ffn_up_bf16<kWaves>, dim3(unit_groups(lo) * (lo.F / (16 * kWaves))), dim3(64 * kWaves), st, tm,
                           lo, l, bbuf, sv, hb);
         else
-            launch_kernel(ffn_up_bf16<1>, dim3(lo.max_units * (lo.F / 16)), dim3(64), st, tm, lo, l, bbuf, sv, hb);
+            launch_kernel(ffn_up_bf16<1>, dim3(unit_groups(lo) * (lo.F / 16)), dim3(64), st, tm, lo, l, bbuf, sv, hb);
     } else {
         launch_kernel(ffn_up_f32, dim3(lo.N * (lo.F / 64)), dim3(64), st, tm, lo, l, bbuf, sv, round,
                       static_cast<const float*>(h));
@@ -688,10 +707,10 @@ hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, int round,
     if (lo.dtype == 1) {
         const int dtn = lo.d / 32;
         if (lo.ffn_waves == kWaves)
-            launch_kernel(ffn_down_bf16<kWaves>, dim3(lo.max_units * ((dtn + kWaves - 1) / kWaves)), dim3(64 * kWaves),
+            launch_kernel(ffn_down_bf16<kWaves>, dim3(unit_groups(lo) * ((dtn + kWaves - 1) / kWaves)), dim3(64 * kWaves),
                           st, tm, lo, l, bbuf, sv);
         else
-            launch_kernel(ffn_down_bf16<1>, dim3(lo.max_units * dtn), dim3(64), st, tm, lo, l, bbuf, sv);
+            launch_kernel(ffn_down_bf16<1>, dim3(unit_groups(lo) * dtn), dim3(64), st, tm, lo, l, bbuf, sv);
     } else {
         launch_kernel(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), st, tm, lo, l, bbuf, sv, round);
     }
