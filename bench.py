@@ -206,14 +206,14 @@ def paper_context(w):
     return out
 
 
-def run_config(w, inputs, warmup, steps, profile_fill=False):
+def run_config(w, inputs, warmup, steps, profile_fill=False, fills=None):
     """One configuration through the C ABI: untimed warm-up tokens, then
     `steps` timed tokens.  Returns (seconds per token, stats, fill ms, fill
     launches)."""
     import torch
 
     from paper_2609_04895_amd.workload import engine_for
-    eng = engine_for(w, inputs, warmup_tokens=warmup)
+    eng = engine_for(w, inputs, warmup_tokens=warmup, fills=fills)
     hidden = inputs["hidden"]
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
     for t in range(warmup):
@@ -242,7 +242,8 @@ def overlap_study(w, warmup, steps):
 
     Configurations on the same inputs: A = the workload (full mode, demand and
     proactive loads; proactive copies on the side stream overlap the previous
-    layer's FFN), B = update-only (demand loads only, all on the critical
+    layer's FFN), A_main = the same with the proactive copies in the demand
+    fill launch on the main stream (no overlap), B = update-only (demand loads only, all on the critical
     path), Z = capacity N (after warm-up nearly every expert stays resident:
     the compute time of the same decode).  c_exp, the time of one expert copy,
     and the launch cost of a fill with nothing to copy, solve fill time =
@@ -255,9 +256,10 @@ def overlap_study(w, warmup, steps):
     cfgB = w.replace(mode=synth.MODE_TEMPORAL, R=0)
     cfgZ = w.replace(mode=synth.MODE_TEMPORAL, R=0, C=w.N)
     res = {}
-    for name, cw, prof in (("A", cfgA, False), ("B", cfgB, False), ("B_fill_events", cfgB, True),
-                           ("Z", cfgZ, False), ("Z_fill_events", cfgZ, True)):
-        sec, tot, fill_ms, fill_n = run_config(cw, inputs, warmup, steps, profile_fill=prof)
+    for name, cw, prof, fills in (("A", cfgA, False, "side"), ("A_main", cfgA, False, "main"), ("B", cfgB, False, None),
+                                  ("B_fill_events", cfgB, True, None), ("Z", cfgZ, False, None),
+                                  ("Z_fill_events", cfgZ, True, None)):
+        sec, tot, fill_ms, fill_n = run_config(cw, inputs, warmup, steps, profile_fill=prof, fills=fills)
         A_, D_, P_, Tc = tot["accesses"], tot["demand_misses"], tot["proactive_loads"], tot["tokens"]
         res[name] = {"ms_per_token": sec * 1e3, "A": A_, "D": D_, "P": P_, "T": Tc,
                      "phys_fills": tot["phys_fills"], "hit": 1 - D_ / A_, "adj_hit": (A_ - D_) / (A_ + P_),
@@ -274,7 +276,7 @@ def overlap_study(w, warmup, steps):
     out = {"study": "transfer overlap (Appendix B.3)", "workload": describe(w), "warmup": warmup, "steps": steps,
            "expert_bytes": w.expert_bytes, "c_exp_ms": c_exp, "copy_GBs": w.expert_bytes / (c_exp / 1e3) / 1e9,
            "empty_fill_launch_ms": t0, "compute_ms_per_token": compute, "configs": res}
-    for name in ("A", "B"):
+    for name in ("A", "A_main", "B"):
         r = res[name]
         exposed = r["ms_per_token"] - compute
         lo_, hi_ = r["D"] * c_exp / r["T"], (r["D"] + r["P"]) * c_exp / r["T"]
