@@ -72,8 +72,7 @@ def describe(w):
 def fills_label(w, fills):
     if not w.has_spatio or w.R == 0:
         return "none (no refinement)"
-    side = fills == "side" or (fills == "auto" and w.pool_kind == 1)
-    return "side stream" if side else "main stream, in the demand fill launch"
+    return "side stream" if fills == "side" else "main stream, in the demand fill launch"
 
 
 def cpu_baseline(w, budget_s, max_procs=16):
@@ -303,8 +302,8 @@ def main():
     ap.add_argument("--arena-slots", type=int, default=None,
                     help="HBM expert slots per layer (default 0: min(N, S C), which holds the union of the caches)")
     ap.add_argument("--fills", choices=["auto", "main", "side"], default="auto",
-                    help="where proactive fills run (auto: the library's choice, the side stream for a host pool "
-                         "and one launch with the demand fill otherwise)")
+                    help="where proactive fills run (auto: the library's choice, one launch with the demand fill "
+                         "on the main stream)")
     ap.add_argument("--ffn-shape", choices=["auto", "single", "grouped"], default="auto",
                     help="bf16 FFN workgroups: one wavefront each, or four sharing big units' activations "
                          "(auto: the library's choice from the average tokens per expert)")

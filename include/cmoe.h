@@ -92,11 +92,11 @@ typedef enum {
 
 /* flags.  Demand fills always run on the main stream: they gate the layer's
  * FFN.  The proactive fills of layer l + 1 follow layer l's cache step: by
- * default they run on the side stream (overlapping layer l's FFN) when the
- * cold pool is in host memory, and otherwise join layer l's demand fill launch
- * on the main stream.  Both flags: CMOE_ERR_INVALID_ARG. */
-#define CMOE_FLAG_FILL_ON_MAIN 0x1u /* proactive fills on the main stream, also for a host pool */
-#define CMOE_FLAG_FILL_ON_SIDE 0x8u /* proactive fills on the side stream, also for a device pool */
+ * default they join layer l's demand fill launch on the main stream; with
+ * CMOE_FLAG_FILL_ON_SIDE (and a side stream) they run on the side stream,
+ * overlapping layer l's FFN.  Both flags: CMOE_ERR_INVALID_ARG. */
+#define CMOE_FLAG_FILL_ON_MAIN 0x1u /* proactive fills on the main stream (the default)      */
+#define CMOE_FLAG_FILL_ON_SIDE 0x8u /* proactive fills on the side stream                    */
 /* bf16 expert FFN launch shape.  Single: one wavefront per workgroup, each on
  * its own row tile.  Grouped: four wavefronts per workgroup on consecutive row
  * tiles of one work unit; units of more than 16 tokens load their activations

@@ -1,5 +1,5 @@
 """Parity at the workloads' full sizes, in the launch configuration bench.py
-times (side stream for proactive fills, all streams, all layers).
+times (all streams, all layers, proactive fills where the library puts them).
 
 The oracle replays the sampled streams {0, S-1} from the host twin's inputs
 (streams never interact in the logical cache path, so a stream replayed alone
@@ -22,12 +22,12 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 
-def run_full(w, T, ffn_samples=8, seed=0):
+def run_full(w, T, ffn_samples=8, seed=0, fills=None):
     from paper_2609_04895_amd import cmoe as B
     from paper_2609_04895_amd.workload import engine_for
     say(f"full-size parity {w.name}: L={w.L} N={w.N} K={w.K} d={w.d} F={w.F} C={w.C} R={w.R} S={w.S}, {T} tokens")
     inp = synth.device_inputs(w, T=T)
-    eng = engine_for(w, inp)
+    eng = engine_for(w, inp, fills=fills)
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
     streams = [0, w.S - 1] if w.S > 1 else [0]
     WR, WT, WS = host_routers(w)
@@ -149,11 +149,12 @@ def test_full_size_qwen3_235b_slice_host_pool():
 
     The full 16-layer pool is 77.3 GB, above what one process can pin on the
     test machine, so the test keeps as many layers as fit (14: 67.6 GB), every
-    other dimension at full size."""
+    other dimension at full size.  Proactive copies run on the side stream,
+    overlapping the FFN (the default joins them to the demand fill)."""
     w = synth.WORKLOADS["qwen3_235b_slice"]
     L = min(w.L, PINNED_LIMIT_BYTES // (w.N * w.expert_bytes))
     assert L == 14
-    run_full(w.replace(L=L), T=8, ffn_samples=4)
+    run_full(w.replace(L=L), T=8, ffn_samples=4, fills="side")
 
 
 def test_full_size_qwen3_30b_single_stream_pinned_pool():

@@ -20,3 +20,9 @@ pytestmark = pytest.mark.gpu
 ], ids=["qwen3_30b", "qwen3_30b_zipf", "gptoss_20b", "qwen3_30b_s1"])
 def test_long_run_full_size(name, repl, T, seed):
     run_full(synth.WORKLOADS[name].replace(**repl), T=T, ffn_samples=12, seed=seed)
+
+
+def test_long_run_single_stream_side_stream_fills():
+    """One stream with its pool in pinned host memory, every proactive load a
+    real copy, the proactive copies on the side stream overlapping the FFN."""
+    run_full(synth.WORKLOADS["qwen3_30b_s1"], T=64, ffn_samples=8, seed=9, fills="side")

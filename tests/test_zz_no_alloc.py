@@ -58,6 +58,26 @@ def test_noalloc_matches_step_two_calls_in_a_row(first, second):
         eb.cmoe_destroy()
 
 
+def test_noalloc_with_a_capacity_limited_arena():
+    """Six HBM slots per layer for a union of up to 32 experts: the FFN runs
+    in rounds, whose plan and work units live in the scratch array too."""
+    from paper_2609_04895_amd import cmoe as B
+    from paper_2609_04895_amd.workload import engine_for
+    w = small(24, True).replace(arena_slots=6)
+    T = 4
+    inp = synth.device_inputs(w, T=T)
+    ea = engine_for(w, inp)
+    eb = engine_for(w, inp, workspace=False)
+    ya = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
+    yb = torch.empty_like(ya)
+    for t in range(T):
+        ea.cmoe_step(inp["hidden"][t], ya)
+        eb.cmoe_step_noalloc(inp["hidden"][t], yb)
+        compare(B, ea, eb, ya, yb, f"arena of 6 slots, token {t}")
+    ea.cmoe_destroy()
+    eb.cmoe_destroy()
+
+
 def test_noalloc_and_step_interleaved_on_one_handle():
     """A handle with a workspace may take either entry point token by token
     (L = 3 is odd, so the bucket buffers change parity between tokens)."""
