@@ -484,6 +484,11 @@ def main():
         copy_gbs = 5 * 2 * (1 << 30) / (c0.elapsed_time(c1) / 1e3) / 1e9
         res["roofline"]["device_copy_GBs"] = copy_gbs
         res["roofline"]["frac_of_device_copy"] = res["roofline"]["achieved"] / copy_gbs
+        # third reference: the practical ceiling of a weight stream, a 1 GiB
+        # read with the FFN's load pattern (cmoe_read_probe), best of 5
+        ceil_gbs = B.cmoe_read_probe(src.view(torch.uint8), reps=5)
+        res["roofline"]["read_ceiling_GBs"] = ceil_gbs
+        res["roofline"]["frac_of_read_ceiling"] = res["roofline"]["achieved"] / ceil_gbs
         del src, dst
     if args.calibrate_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")   # 1 GiB

@@ -310,6 +310,20 @@ cmoe_status cmoe_profile_end(cmoe_handle* hd, double* ms_out, int64_t* launches_
  * All zeros before any counted token.  Synchronizes. */
 cmoe_status cmoe_concentration(cmoe_handle* hd, int32_t top_m, double* out4);
 
+/* Measurement utility, not part of the decode path: the rate at which the
+ * current device streams `bytes` of device memory at src with the access
+ * pattern of the expert weight loads (16-byte nontemporal loads, one
+ * contiguous kilobyte per wavefront instruction, eight in flight, each
+ * wavefront walking its own contiguous block).  It is the practical ceiling of
+ * the FFN's weight stream, as opposed to the datasheet peak.  src: device
+ * memory owned by the caller, only read (its contents do not matter);
+ * bytes >= 64 MiB (a smaller buffer cannot occupy the device); the part read
+ * is the largest multiple of the probe's block size that fits.  Runs `reps`
+ * >= 1 launches on the null stream of the current device, synchronizes, and
+ * writes the best rate in GB/s (10^9 bytes per second) to *gbps.  Allocates
+ * nothing. */
+cmoe_status cmoe_read_probe(const void* src, int64_t bytes, int32_t reps, double* gbps);
+
 const char* cmoe_last_error(void);
 
 #ifdef __cplusplus

@@ -55,7 +55,7 @@ KERNEL_NAMES = ("router", "cache_step", "fill", "ffn_up", "ffn_down", "combine")
 
 EXPORTED = ("cmoe_query", "cmoe_init", "cmoe_step", "cmoe_step_noalloc", "cmoe_step_logits", "cmoe_stats", "cmoe_get_cache",
             "cmoe_set_cache", "cmoe_set_R", "cmoe_reset", "cmoe_destroy", "cmoe_view_bytes", "cmoe_read",
-            "cmoe_profile_begin", "cmoe_profile_end", "cmoe_concentration", "cmoe_last_error")
+            "cmoe_profile_begin", "cmoe_profile_end", "cmoe_concentration", "cmoe_read_probe", "cmoe_last_error")
 
 
 class cmoe_config(ctypes.Structure):
@@ -122,6 +122,7 @@ def lib():
         L.cmoe_profile_begin.argtypes = [vp, i32, ctypes.c_uint32]
         L.cmoe_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_double), i64p]
         L.cmoe_concentration.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double)]
+        L.cmoe_read_probe.argtypes = [vp, ctypes.c_int64, i32, ctypes.POINTER(ctypes.c_double)]
         L.cmoe_last_error.argtypes = []
         L.cmoe_last_error.restype = ctypes.c_char_p
         for n in EXPORTED:
@@ -156,6 +157,15 @@ def cmoe_query(cfg: cmoe_config) -> cmoe_sizes:
     out = cmoe_sizes()
     _check(lib().cmoe_query(ctypes.byref(cfg), ctypes.byref(out)))
     return out
+
+
+def cmoe_read_probe(buf, reps: int = 5) -> float:
+    """GB/s of the device's streaming read of the device tensor buf (at
+    least 64 MiB) with the expert weight loads' access pattern."""
+    rate = ctypes.c_double()
+    _check(lib().cmoe_read_probe(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(), reps,
+                                 ctypes.byref(rate)))
+    return rate.value
 
 
 def _ptr(t) -> Optional[int]:

@@ -810,6 +810,34 @@ cmoe_status cmoe_concentration(cmoe_handle* hd, int32_t top_m, double* out4) {
     return CMOE_OK;
 }
 
+cmoe_status cmoe_read_probe(const void* src, int64_t bytes, int32_t reps, double* gbps) {
+    if (!src || !gbps) return fail(CMOE_ERR_INVALID_ARG, "read probe: src and gbps are required");
+    if (reps < 1) return fail(CMOE_ERR_INVALID_ARG, "read probe: reps must be >= 1");
+    if (bytes < ((int64_t)64 << 20)) return fail(CMOE_ERR_INVALID_ARG, "read probe: needs a buffer of at least 64 MiB");
+    int64_t read = 0;
+    const int64_t per_wave = cmoe::read_probe_units_per_wave(bytes, &read);
+    cmoe_handle* hd = nullptr;  // no handle: errors do not mark one broken
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    hipError_t e = hipEventCreate(&e0);
+    if (e == hipSuccess) e = hipEventCreate(&e1);
+    float best = 0.0f;
+    for (int32_t r = 0; e == hipSuccess && r < reps; ++r) {
+        cmoe::Timing tm;
+        tm.start = e0;
+        tm.stop = e1;
+        e = cmoe::launch_read_probe(src, per_wave, nullptr, tm);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float ms = 0.0f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+        if (e == hipSuccess && (best == 0.0f || ms < best)) best = ms;
+    }
+    if (e1) (void)hipEventDestroy(e1);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e != hipSuccess) return hip_fail(hd, e, "read probe");
+    *gbps = (double)read / (best * 1e-3) / 1e9;
+    return CMOE_OK;
+}
+
 const char* cmoe_last_error(void) { return g_err.c_str(); }
 
 }  // extern "C"

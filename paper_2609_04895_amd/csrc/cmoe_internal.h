@@ -135,5 +135,10 @@ hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, int round, c
 hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, int round, hipStream_t st,
                            const Timing& tm = {});
 hipError_t launch_combine(const Layout& lo, int l, float* y, hipStream_t st, const Timing& tm = {});
+// streaming read of per_wave 16-byte units by each wavefront of the probe
+// grid; read_probe_units_per_wave gives the largest per_wave that fits in
+// `bytes` and the bytes the grid then reads
+int64_t read_probe_units_per_wave(int64_t bytes, int64_t* read_bytes);
+hipError_t launch_read_probe(const void* src, int64_t per_wave, hipStream_t st, const Timing& tm);
 
 }  // namespace cmoe

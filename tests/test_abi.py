@@ -148,3 +148,17 @@ def test_null_handle_calls_fail_cleanly():
     assert L.cmoe_reset(None) == B.CMOE_ERR_INVALID_ARG
     assert L.cmoe_destroy(None) == B.CMOE_OK
     assert L.cmoe_view_bytes(None, 0) == 0
+
+
+@pytest.mark.parametrize("src,nbytes,reps,out,msg", [
+    (None, 1 << 30, 1, True, "required"),            # no buffer
+    (1 << 20, 1 << 30, 1, False, "required"),        # no output
+    (1 << 20, 1 << 30, 0, True, "reps"),             # no launch asked for
+    (1 << 20, (64 << 20) - 1, 1, True, "64 MiB"),    # too small to occupy the device
+])
+def test_read_probe_rejects_bad_arguments_before_any_launch(src, nbytes, reps, out, msg):
+    rate = ctypes.c_double(-1.0)
+    st = B.lib().cmoe_read_probe(ctypes.c_void_p(src), nbytes, reps, ctypes.byref(rate) if out else None)
+    assert st == B.CMOE_ERR_INVALID_ARG
+    assert msg in B.lib().cmoe_last_error().decode()
+    assert rate.value == -1.0
