@@ -1,11 +1,12 @@
 """Parity at the workloads' full sizes, in the launch configuration bench.py
 times (all streams, all layers, proactive fills where the library puts them).
 
-The oracle replays the sampled streams {0, S-1} from the host twin's inputs
-(streams never interact in the logical cache path, so a stream replayed alone
-is exact): logits within one ulp, decisions, per-token events and the
-per-(stream, layer) counters bit for bit, and FFN outputs of sampled
-(stream, token, layer) triples within the bf16 tolerance.  For all streams the
+The oracle replays streams 0 and S-1 and two seeded streams between them
+from the host twin's inputs (streams never interact in the logical cache
+path, so a stream replayed alone is exact): logits within one ulp,
+decisions, per-token events and the per-(stream, layer) counters bit for
+bit, and FFN outputs of sampled (stream, token, layer) triples within the
+bf16 tolerance.  For all streams the
 invariants that hold at any size are checked on every token: hits + demand
 misses = K, |C| <= capacity, proactive loads <= R (= 0 in update-only mode),
 traffic = (D + P) x expert bytes, physical fills <= D + P.
@@ -15,11 +16,21 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import host_routers, oracle_logits, oracle_run, rel_err, say, split_slots
+from gpu_util import host_routers, oracle_logits, oracle_run, rel_err, say, split_slots, stable_seed
 
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
+
+
+def replay_streams(w, n_mid=2):
+    """The streams the oracle replays: the first, the last and n_mid seeded
+    ones between them (the same on every run)."""
+    if w.S <= 2:
+        return list(range(w.S))
+    rng = np.random.default_rng(stable_seed(f"replay streams {w.name} S={w.S}"))
+    mid = rng.choice(np.arange(1, w.S - 1), size=min(n_mid, w.S - 2), replace=False)
+    return sorted({0, w.S - 1, *(int(s) for s in mid)})
 
 
 def run_full(w, T, ffn_samples=8, seed=0, fills=None):
@@ -29,7 +40,8 @@ def run_full(w, T, ffn_samples=8, seed=0, fills=None):
     inp = synth.device_inputs(w, T=T)
     eng = engine_for(w, inp, fills=fills)
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
-    streams = [0, w.S - 1] if w.S > 1 else [0]
+    streams = replay_streams(w)
+    say(f"  replayed streams {streams}")
     WR, WT, WS = host_routers(w)
     bias = synth.zipf_bias(w)
     H = {(s, l): synth.hidden_host(w, s, l, T=T) for s in streams for l in range(w.L)}
@@ -48,8 +60,8 @@ def run_full(w, T, ffn_samples=8, seed=0, fills=None):
     for t in range(T):
         eng.cmoe_step(inp["hidden"][t], y)
         zg_all = eng.cmoe_read(B.CMOE_VIEW_LOGITS)               # [L][S][n_r][N]
-        zg = zg_all[:, streams].transpose(1, 0, 2, 3)            # [2][L][n_r][N]
-        ref = oracle_logits(w, WR, WT, WS, bias, H, t, streams)   # [2][L][n_r][N]
+        zg = zg_all[:, streams].transpose(1, 0, 2, 3)            # [streams][L][n_r][N]
+        ref = oracle_logits(w, WR, WT, WS, bias, H, t, streams)   # [streams][L][n_r][N]
         d = zg != ref
         if d.any():
             gap = np.abs(zg.astype(np.float64) - ref)
