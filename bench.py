@@ -179,6 +179,22 @@ def cpu_baseline(w, budget_s, max_procs=16):
     return res
 
 
+def topk_near_ties(z, K):
+    """Top-K boundary of the native logits z [L][S][N] (fp32, the last timed
+    token): how many (layer, stream) pairs have their K-th and (K+1)-th
+    largest logits equal, or one fp32 ulp apart, where a one-ulp difference
+    from the fp64 sum could decide the selection."""
+    import numpy as np
+    pairs = z.shape[0] * z.shape[1]
+    if K >= z.shape[-1]:
+        return {"pairs": pairs, "equal": 0, "within_one_ulp": 0}
+    zs = -np.sort(-z.astype(np.float32), axis=-1)
+    kth, nxt = zs[..., K - 1], zs[..., K]
+    gap = kth - nxt
+    return {"pairs": pairs, "equal": int(np.sum(gap == 0)),
+            "within_one_ulp": int(np.sum(gap <= np.spacing(np.abs(kth))))}
+
+
 def paper_context(w):
     """The paper's own hit-rate and traffic figures for the method and backbone
     this workload stands in for (Tables 1 and 3, Section 4.1 metrics), quoted
@@ -396,6 +412,7 @@ def main():
     elapsed = ev0.elapsed_time(ev1) / 1e3
     tot, _, _ = eng.cmoe_stats()
     active = eng.cmoe_read(B.CMOE_VIEW_ACTIVE)
+    near_ties = topk_near_ties(eng.cmoe_read(B.CMOE_VIEW_LOGITS)[:, :, 0], w.K)
     print(f"[bench] timed region {elapsed * 1e3:.1f} ms (wall {wall * 1e3:.1f} ms)", file=sys.stderr, flush=True)
 
     e = w.elem_bytes
@@ -462,7 +479,8 @@ def main():
     A, D, P, Tc = tot["accesses"], tot["demand_misses"], tot["proactive_loads"], tot["tokens"]
     res["cache"] = {"hit": 1 - D / A, "adj_hit": (A - D) / (A + P), "load_mb_per_token": (D + P) * w.expert_bytes
                     / 1e6 / Tc, "accesses": A, "demand_misses": D, "proactive_loads": P, "tokens": Tc,
-                    "phys_fills": tot["phys_fills"], "distinct_experts_per_layer_step": n_act / launches}
+                    "phys_fills": tot["phys_fills"], "distinct_experts_per_layer_step": n_act / launches,
+                    "topk_near_ties_last_token": near_ties}
     eff, ent, fmax, top8 = eng.cmoe_concentration(8)
     res["concentration"] = {"effective_experts": eff, "entropy_nats": ent, "max_frequency": fmax, "top8_mass": top8}
     res["paper_context"] = paper_context(w)
