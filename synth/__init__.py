@@ -142,14 +142,14 @@ def normal_host_bf16_bits(seed: int, tid: int, n: int, scale: float) -> np.ndarr
 
 def router_host(w: Workload, kind: int, layer: int) -> np.ndarray:
     """Router weights of one layer as stored values, float32 [N][d]."""
-    v = normal_host(w.seed, router_tid(kind, layer), w.N * w.d, weight_scale(w), w.dtype == DTYPE_BF16)
+    v = normal_host(w.seed, router_tid(kind, w.layer0 + layer), w.N * w.d, weight_scale(w), w.dtype == DTYPE_BF16)
     return v.reshape(w.N, w.d)
 
 
 def expert_host(w: Workload, layer: int, expert: int):
     """(W_gate[F][d], W_up[F][d], W_down[d][F]) of one expert as float32."""
     fd = w.F * w.d
-    v = normal_host(w.seed, expert_tid(w, layer, expert), 3 * fd, weight_scale(w),
+    v = normal_host(w.seed, expert_tid(w, w.layer0 + layer, expert), 3 * fd, weight_scale(w),
                     w.dtype == DTYPE_BF16)
     return v[:fd].reshape(w.F, w.d), v[fd:2 * fd].reshape(w.F, w.d), v[2 * fd:].reshape(w.d, w.F)
 
@@ -160,7 +160,7 @@ def hidden_host(w: Workload, stream: int, layer: int, T: Optional[int] = None) -
     T = w.T if T is None else T
     rho, c0 = ar1_params(w)
     out = np.empty(T * w.d, dtype=np.float32)
-    lib.syn_ar1_f32(lib.syn_key(w.seed, hidden_tid(stream, layer)), T, w.d, rho, c0, unit_scale(),
+    lib.syn_ar1_f32(lib.syn_key(w.seed, hidden_tid(stream, w.layer0 + layer)), T, w.d, rho, c0, unit_scale(),
                     int(w.dtype == DTYPE_BF16), _f32_ptr(out))
     return out.reshape(T, w.d)
 
@@ -178,7 +178,7 @@ def zipf_bias(w: Workload) -> Optional[np.ndarray]:
     lib = _load_cpu()
     out = np.empty((w.L, w.N), dtype=np.float32)
     for l in range(w.L):
-        key = lib.syn_key(w.seed, (KIND_ZIPF << 56) + l)
+        key = lib.syn_key(w.seed, (KIND_ZIPF << 56) + w.layer0 + l)
         perm = list(range(w.N))
         for i in range(w.N - 1, 0, -1):
             j = int(lib.syn_draw(key, i) % (i + 1))
@@ -202,7 +202,7 @@ def _check(rc: int, what: str):
 
 def fill_router_dev(w: Workload, kind: int, out_ptr: int, stream: int = 0):
     """Fills [L][N][d] router weights of one kind at a device address."""
-    _check(_load_hip().syn_dev_fill(w.seed, router_tid(kind, 0), 1, w.L, w.N * w.d, weight_scale(w),
+    _check(_load_hip().syn_dev_fill(w.seed, router_tid(kind, w.layer0), 1, w.L, w.N * w.d, weight_scale(w),
                                     int(w.dtype == DTYPE_BF16), out_ptr, stream), "router")
 
 
@@ -213,7 +213,7 @@ def fill_pool_dev(w: Workload, out_ptr: int, stream: int = 0, layers: Optional[T
     points at layer l0), so a pool in host memory can be built in chunks.
     """
     l0, l1 = (0, w.L) if layers is None else layers
-    _check(_load_hip().syn_dev_fill(w.seed, expert_tid(w, l0, 0), 1, (l1 - l0) * w.N,
+    _check(_load_hip().syn_dev_fill(w.seed, expert_tid(w, w.layer0 + l0, 0), 1, (l1 - l0) * w.N,
                                     3 * w.F * w.d, weight_scale(w), int(w.dtype == DTYPE_BF16),
                                     out_ptr, stream), "pool")
 
@@ -222,7 +222,7 @@ def fill_hidden_dev(w: Workload, out_ptr: int, T: Optional[int] = None, stream: 
     """Fills AR(1) hidden states, token-major [T][S][L][d], at a device address."""
     T = w.T if T is None else T
     rho, c0 = ar1_params(w)
-    _check(_load_hip().syn_dev_ar1(w.seed, hidden_tid(0, 0), 1 << 24, 1, w.S, w.L, w.d, T, rho, c0,
+    _check(_load_hip().syn_dev_ar1(w.seed, hidden_tid(0, w.layer0), 1 << 24, 1, w.S, w.L, w.d, T, rho, c0,
                                    unit_scale(), int(w.dtype == DTYPE_BF16), out_ptr, stream), "hidden")
 
 

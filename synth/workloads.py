@@ -57,6 +57,8 @@ class Workload:
     policy: int = POLICY_ROUTER
     lrfu_lambda: float = 0.5
     arena_slots: int = 0              # HBM expert slots per layer (0: min(N, S C))
+    layer0: int = 0                   # model layer of layer 0: a workload of L layers covers layers
+                                      # layer0 .. layer0 + L - 1 of the model (their own weights and inputs)
 
     @property
     def elem_bytes(self) -> int:

@@ -36,7 +36,8 @@ def replay_streams(w, n_mid=2):
 def run_full(w, T, ffn_samples=8, seed=0, fills=None):
     from paper_2609_04895_amd import cmoe as B
     from paper_2609_04895_amd.workload import engine_for
-    say(f"full-size parity {w.name}: L={w.L} N={w.N} K={w.K} d={w.d} F={w.F} C={w.C} R={w.R} S={w.S}, {T} tokens")
+    say(f"full-size parity {w.name}: L={w.L} (model layers {w.layer0}..{w.layer0 + w.L - 1}) N={w.N} K={w.K} "
+        f"d={w.d} F={w.F} C={w.C} R={w.R} S={w.S}, {T} tokens")
     inp = synth.device_inputs(w, T=T)
     eng = engine_for(w, inp, fills=fills)
     y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device="cuda:0")
@@ -167,6 +168,18 @@ def test_full_size_qwen3_235b_slice_host_pool():
     L = min(w.L, PINNED_LIMIT_BYTES // (w.N * w.expert_bytes))
     assert L == 14
     run_full(w.replace(L=L), T=8, ffn_samples=4, fills="side")
+
+
+def test_full_size_qwen3_235b_slice_last_layers_host_pool():
+    """The two layers of the Qwen3-235B-A22B slice that do not fit next to the
+    other 14 in pinned host memory (model layers 14 and 15: their own routers,
+    experts and hidden states) as an engine of their own, so that every layer
+    of the slice passes through the kernels at full size.  Its first layer is
+    refined from its own last layer's prediction, not from model layer 13."""
+    w = synth.WORKLOADS["qwen3_235b_slice"]
+    first = min(w.L, PINNED_LIMIT_BYTES // (w.N * w.expert_bytes))
+    assert first == 14
+    run_full(w.replace(L=w.L - first, layer0=first), T=8, ffn_samples=4)
 
 
 def test_full_size_qwen3_30b_single_stream_pinned_pool():
