@@ -313,7 +313,7 @@ __device__ void refine_one(const Layout& lo, int s, int rl, int R, int t, bool c
     int count = 0;
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
-        cw[j] = cw_in[j];
+        cw[j] = j < lo.NW ? cw_in[j] : 0ull;
         count += __popcll(cw[j]);
     }
     int nP = 0;
@@ -370,30 +370,31 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
 
     // Loads that do not depend on this token's scores are issued first so
     // that their latencies overlap: the refined layer's a^T and cache words,
-    // the accessed layer's cache words.
-    float aTv[NPL];
-    unsigned long long cw_r[NPL], cw_a[NPL];
+    // the accessed layer's cache words and classical priorities, and the
+    // counters.  They are issued whatever the flags (rows clamped into range,
+    // words and experts past the end masked where they are used): a load
+    // under a branch of its own makes the compiler wait for it where the
+    // branches join, before the router partials below are even requested.
     const bool refine = (a.flags & kFlagRefine) != 0;
-    // counters this wavefront updates (lane 0 owns them)
-    int64_t ctr_a[kNctr] = {0, 0, 0, 0, 0}, ctr_rp = 0;
-    if (lane == 0 && counted) {
-        if (a.flags & kFlagAccess) {
-#pragma unroll
-            for (int c = 0; c < kNctr; ++c) ctr_a[c] = lo.ctr[((int64_t)s * L + a.l) * kNctr + c];
-        }
-        if (refine) ctr_rp = lo.ctr[((int64_t)s * L + a.rl) * kNctr + kCtrP];
-    }
-    int64_t bucket = 0;  // lane k < K: bucket of its selection and position in it
-    int bucket_pos = 0;
-    float polv[NPL];  // classical priority of the accessed layer
+    const int64_t row_a = (int64_t)s * L + a.l, row_r = (int64_t)s * L + min(a.rl, L - 1);
+    float aTv[NPL], polv[NPL], pS_st[NPL];
+    unsigned long long cw_r[NPL], cw_a[NPL];
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
-        const int e = j * 64 + lane;
-        aTv[j] = (refine && e < N) ? lo.aT[((int64_t)s * L + a.rl) * N + e] : 0.0f;
-        cw_r[j] = (refine && j < lo.NW) ? lo.cache[((int64_t)s * L + a.rl) * lo.NW + j] : 0ull;
-        cw_a[j] = ((a.flags & kFlagAccess) && j < lo.NW) ? lo.cache[((int64_t)s * L + a.l) * lo.NW + j] : 0ull;
-        polv[j] = (classical && (a.flags & kFlagAccess) && e < N) ? lo.pol[((int64_t)s * L + a.l) * N + e] : 0.0f;
+        const int ec = min(j * 64 + lane, N - 1), jw = min(j, lo.NW - 1);
+        pS_st[j] = lo.pS[(int64_t)s * N + ec];  // the stored prediction, for a refine-only launch
+        aTv[j] = lo.aT[row_r * N + ec];
+        cw_r[j] = lo.cache[row_r * lo.NW + jw];
+        cw_a[j] = lo.cache[row_a * lo.NW + jw];
+        polv[j] = lo.pol[row_a * N + ec];
     }
+    // counters this wavefront updates (lane 0 owns them)
+    int64_t ctr_a[kNctr];
+#pragma unroll
+    for (int c = 0; c < kNctr; ++c) ctr_a[c] = lo.ctr[row_a * kNctr + c];
+    const int64_t ctr_rp = lo.ctr[row_r * kNctr + kCtrP];
+    int64_t bucket = 0;  // lane k < K: bucket of its selection and position in it
+    int bucket_pos = 0;
 
     if (a.flags & kFlagAccess) {
         const int l = a.l;
@@ -512,7 +513,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
 #pragma unroll
             for (int j = 0; j < NPL; ++j) {
                 const bool used = (sw[j] >> lane) & 1ull;
-                float v = polv[j];
+                float v = j * 64 + lane < N ? polv[j] : 0.0f;
                 if (lo.policy == kPolicyLRU) {
                     if (used) v = (float)(2 * a.t + 2);
                 } else if (lo.policy == kPolicyLFU) {
@@ -533,7 +534,7 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
         int count = 0, hits = 0;
 #pragma unroll
         for (int j = 0; j < NPL; ++j) {
-            cw[j] = cw_a[j];
+            cw[j] = j < lo.NW ? cw_a[j] : 0ull;
             count += __popcll(cw[j]);
             hits += __popcll(cw[j] & sw[j]);
         }
@@ -584,15 +585,21 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
                 }
             }
         }
+        // The refinement is called on each side of the branch: after a join
+        // with the refine-only side, whose prediction loads may still be in
+        // flight there, the compiler waits for every outstanding memory
+        // operation, and with it for the bucket atomic issued above, whose
+        // round trip the refinement is meant to hide.
+        if (refine) refine_one<NPL>(lo, s, a.rl, a.R, a.t, counted, pred, aTv, cw_r, ctr_rp, lane);
     } else {
         // refine-only launch: the predecessor's prediction is the stored one
 #pragma unroll
         for (int j = 0; j < NPL; ++j) {
             const int e = j * 64 + lane;
-            pred[j] = e < N ? lo.pS[(int64_t)s * N + e] : 0.0f;
+            pred[j] = e < N ? pS_st[j] : 0.0f;
         }
+        if (refine) refine_one<NPL>(lo, s, a.rl, a.R, a.t, counted, pred, aTv, cw_r, ctr_rp, lane);
     }
-    if (refine) refine_one<NPL>(lo, s, a.rl, a.R, a.t, counted, pred, aTv, cw_r, ctr_rp, lane);
     if ((a.flags & kFlagAccess) && lane < K) {
         lo.pairs[bucket * lo.S + bucket_pos] = (s << 8) | lane;
         if (counted && bucket_pos == 0) atomicAdd(&lo.active_sum[a.l], 1ull);
