@@ -20,24 +20,51 @@ namespace cmoe {
 
 namespace {
 
-// Exclusive prefix sum over the 256 threads of the block; *total gets the sum.
-__device__ int block_scan(int v, int* total, int* lds4) {
+// Threads of a fill workgroup (four wavefronts), a compile-time constant so
+// that no loop bound has to be read from the dispatch packet.
+constexpr int kFillThreads = 256;
+
+// Block-wide exclusive prefix counts and sums over the 256 threads of the
+// block, each with one barrier: the wavefront totals go to a four-entry
+// slot of LDS, and consecutive calls use different slots, so no barrier is
+// needed after one call before the next.  *total gets the block total.
+// Flags: the ballot bits below the lane.
+__device__ int block_count(bool v, int* total, int* slot) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
-    if (lane == 63) lds4[w] = x;
+    const unsigned long long b = __ballot(v);
+    const int below = (int)__builtin_amdgcn_mbcnt_hi((unsigned)(b >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)b, 0u));
+    if (lane == 0) slot[w] = __popcll(b);
     __syncthreads();
     int off = 0, tot = 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        if (i < w) off += lds4[i];
-        tot += lds4[i];
+        if (i < w) off += slot[i];
+        tot += slot[i];
     }
+    *total = tot;
+    return off + below;
+}
+
+// Values: an inclusive wavefront scan in DPP steps (shifts by 1, 2, 4 and 8
+// inside each 16-lane row, then the last lane of row 0 and of row 1 added to
+// the rows after them); a lane whose source is outside its row adds 0.
+__device__ int block_scan(int v, int* total, int* slot) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int x = v;
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);  // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);  // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15 into rows 1, 3
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31 into rows 2, 3
+    if (lane == 63) slot[w] = x;
     __syncthreads();
+    int off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if (i < w) off += slot[i];
+        tot += slot[i];
+    }
     *total = tot;
     return off + x - v;
 }
@@ -126,7 +153,7 @@ __device__ inline unsigned long long cache_word(const Layout& lo, int layer, int
 struct FillLds {
     unsigned long long U[4];
     int so[kMaxN], se[kMaxN], stp[kMaxN], rnd_s[kMaxN], free_list[kMaxN], enter_list[kMaxN], victim_list[kMaxN];
-    int lds4[4];
+    int lds4[4][4];  // block-scan slots
     __align__(16) int key[kMaxN];
     int by_rank[kMaxN], who[kMaxN], m_rank[kMaxN];
 };
@@ -137,7 +164,7 @@ struct FillLds {
 __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs& f, FillLds& sm, int wg, int nwg) {
     unsigned long long* U = sm.U;
     int *so = sm.so, *se = sm.se, *stp = sm.stp, *rnd_s = sm.rnd_s, *free_list = sm.free_list;
-    int *enter_list = sm.enter_list, *victim_list = sm.victim_list, *lds4 = sm.lds4;
+    int *enter_list = sm.enter_list, *victim_list = sm.victim_list, (*lds4)[4] = sm.lds4;
     const int tid = threadIdx.x;
     const int N = lo.N, layer = f.layer, P = lo.n_slots;
     const int64_t vin = (int64_t)f.rv * lo.L + layer, vout = (int64_t)(f.rv ^ 1) * lo.L + layer;
@@ -145,21 +172,24 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
     const int32_t* se_in = lo.slot_exp + vin * P;
     const int32_t* st_in = lo.slot_stamp + vin * P;
     const bool demand = f.kind == 0;
-    // Every global load of the prologue is issued before the first is used:
-    // the slot maps and stamps, the bucket sizes (the executed experts and
-    // the FFN work units), the round plan of a later round, and the first
-    // batch of cache words (indices clamped; a clamped value is not used).
+    // Every global load of the prologue is issued before the first is used,
+    // whatever the event (indices clamped; a value that is not needed is not
+    // used): the slot maps and stamps, the bucket sizes (the executed experts
+    // and the FFN work units), the round plan of a later round, the fill
+    // counters workgroup 0 adds to, and the first batch of cache words.
     const bool units = demand && f.units && wg == 0;
     const int S_NW = lo.S * lo.NW;
     const int so_v = so_in[min(tid, N - 1)];
     const int se_v = se_in[min(tid, P - 1)];
     const int st_v = st_in[min(tid, P - 1)];
-    const int m_v = demand ? lo.bcount[(int64_t)f.bbuf * N + min(tid, N - 1)] : 0;
-    const int ro_v = (demand && f.round > 0) ? lo.round_of[min(tid, N - 1)] : -1;
+    const int mb_v = lo.bcount[(int64_t)f.bbuf * N + min(tid, N - 1)];
+    const int ro_v = lo.round_of[min(tid, N - 1)];
+    const int64_t phys_v = lo.phys[layer * 2 + f.kind];
+    const int32_t sf_v = lo.step_fills[layer * 2];
     constexpr int kWords = 4;  // cache words per thread per batch
     unsigned long long w[kWords];
 #pragma unroll
-    for (int u = 0; u < kWords; ++u) w[u] = cache_word(lo, layer, min(tid + u * (int)blockDim.x, S_NW - 1));
+    for (int u = 0; u < kWords; ++u) w[u] = cache_word(lo, layer, min(tid + u * kFillThreads, S_NW - 1));
     __builtin_amdgcn_sched_barrier(0);
     if (tid < 4) U[tid] = 0ull;
     if (tid < N) so[tid] = so_v;
@@ -168,20 +198,21 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         stp[tid] = st_v;
     }
     __syncthreads();
-    for (int i0 = 0; i0 < S_NW; i0 += kWords * blockDim.x) {
+    for (int i0 = 0; i0 < S_NW; i0 += kWords * kFillThreads) {
         if (i0 > 0) {
 #pragma unroll
             for (int u = 0; u < kWords; ++u)
-                w[u] = cache_word(lo, layer, min(i0 + tid + u * (int)blockDim.x, S_NW - 1));
+                w[u] = cache_word(lo, layer, min(i0 + tid + u * kFillThreads, S_NW - 1));
             __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
         for (int u = 0; u < kWords; ++u) {
-            const int i = i0 + tid + u * blockDim.x;
+            const int i = i0 + tid + u * kFillThreads;
             if (i < S_NW && w[u]) atomicOr(&U[i % lo.NW], w[u]);
         }
     }
     __syncthreads();
+    const int m_v = demand ? mb_v : 0;
     const int e = tid;
     const bool inU = e < N && ((U[e >> 6] >> (e & 63)) & 1ull);
     int cur = e < N ? so[e] : -1;
@@ -206,8 +237,8 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         } else if (f.round == 0) {
             const bool res_e = inE && cur >= 0, mis_e = inE && cur < 0;
             int nres, nmis;
-            const int r1 = block_scan(res_e ? 1 : 0, &nres, lds4);
-            const int r2 = block_scan(mis_e ? 1 : 0, &nmis, lds4);
+            const int r1 = block_count(res_e, &nres, lds4[0]);
+            const int r2 = block_count(mis_e, &nmis, lds4[1]);
             rnd = res_e ? r1 / P : (mis_e ? (nres + r2) / P : -1);
         } else {
             rnd = e < N ? ro_v : -1;
@@ -221,9 +252,9 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
     else enter = now && cur < 0;
     const bool is_free = tid < P && se[tid] == -1;
     int nfree, nenter;
-    const int rf = block_scan(is_free ? 1 : 0, &nfree, lds4);
+    const int rf = block_count(is_free, &nfree, lds4[2]);
     if (is_free) free_list[rf] = tid;
-    const int re = block_scan(enter ? 1 : 0, &nenter, lds4);
+    const int re = block_count(enter, &nenter, lds4[3]);
     // A round that needs more than the free slots evicts the least recently
     // used experts that no remaining round needs (lower slot on ties), ranked
     // by (stamp, slot); after refinement only free slots are filled.
@@ -278,11 +309,11 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         if (demand && f.round == 0 && tid < N) lo.round_of[tid] = rnd;
         if (tid == 0) {
             if (demand && f.round > 0)
-                lo.step_fills[layer * 2] += nent;
+                lo.step_fills[layer * 2] = sf_v + nent;
             else
                 lo.step_fills[layer * 2 + f.kind] = nent;
             if (f.zero_pre) lo.step_fills[layer * 2 + 1] = 0;
-            if (f.counted) lo.phys[layer * 2 + f.kind] += nent;
+            if (f.counted) lo.phys[layer * 2 + f.kind] = phys_v + nent;
         }
     }
     // FFN work units of this round: each of its experts' buckets cut into
@@ -295,8 +326,8 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
     const int ut = lo.unit_tokens;
     const bool multi = __syncthreads_or(units && m_own > ut) != 0;
     if (units && !multi) {
-        // blockDim.x >= N: thread e holds expert e's bucket size
-        for (int i = tid; i < lo.max_units; i += blockDim.x)
+        // kFillThreads >= N: thread e holds expert e's bucket size
+        for (int i = tid; i < lo.max_units; i += kFillThreads)
             unit4[i] = (i < N && m_own > 0) ? int4{i, so[i], m_own, 0} : int4{-1, -1, 0, 0};
     } else if (units) {
         // otherwise experts with more tokens go first (lower index on ties),
@@ -305,7 +336,7 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         int *key = sm.key, *by_rank = sm.by_rank, *who = sm.who, *m_rank = sm.m_rank;
         const int m = m_own;
         const int mykey = (m << 8) | (255 - tid);
-        key[tid] = tid < N ? mykey : -1;  // blockDim.x == kMaxN: every entry is written
+        key[tid] = tid < N ? mykey : -1;  // kFillThreads == kMaxN: every entry is written
         __syncthreads();
         int rank = 0;
         if (tid < N) {
@@ -323,19 +354,19 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         __syncthreads();
         const int passes = tid < N ? by_rank[tid] : 0;
         int total;
-        const int off = block_scan(passes, &total, lds4);
+        const int off = block_scan(passes, &total, lds4[0]);
         if (tid < N) {
             const int e = who[tid];
             for (int q = 0; q < passes; ++q)
                 unit4[off + q] = int4{(q << 8) | e, so[e], min(ut, m_rank[tid] - ut * q), 0};
         }
-        for (int i = total + tid; i < lo.max_units; i += blockDim.x) unit4[i] = int4{-1, -1, 0, 0};
+        for (int i = total + tid; i < lo.max_units; i += kFillThreads) unit4[i] = int4{-1, -1, 0, 0};
     }
     if (nent == 0) return;
     const int64_t bytes = lo.expert_elems * (lo.dtype == 1 ? 2 : 4);
     const int64_t n16 = bytes / 16;
-    const int64_t gid = (int64_t)wg * blockDim.x + tid;
-    const int64_t gs = (int64_t)nwg * blockDim.x;
+    const int64_t gid = (int64_t)wg * kFillThreads + tid;
+    const int64_t gs = (int64_t)nwg * kFillThreads;
     for (int k = 0; k < nent; ++k) {
         const int ex = enter_list[k];
         if (ex < 0) continue;
@@ -379,7 +410,7 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
 // demand event of one layer and the proactive event of the next, which both
 // follow the same cache step, in one launch, each on half the workgroups
 // (even ones: f, odd ones: g).
-__global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f, FillArgs g) {
+__global__ __launch_bounds__(kFillThreads) void fill_kernel(Layout lo, FillArgs f, FillArgs g) {
     __shared__ FillLds sm;
     if (g.layer < 0)
         residency_event(lo, f, sm, blockIdx.x, gridDim.x);
@@ -394,7 +425,7 @@ __global__ __launch_bounds__(256) void fill_kernel(Layout lo, FillArgs f, FillAr
 hipError_t launch_fill(const Layout& lo, const FillArgs& f, const FillArgs* g, hipStream_t st, const Timing& tm) {
     FillArgs none{};
     none.layer = -1;
-    launch_kernel(fill_kernel, dim3(lo.pool_host ? kFillBlocksHost : kFillBlocksDevice), dim3(256), st, tm, lo, f,
+    launch_kernel(fill_kernel, dim3(lo.pool_host ? kFillBlocksHost : kFillBlocksDevice), dim3(kFillThreads), st, tm, lo, f,
                   g ? *g : none);
     return hipGetLastError();
 }
