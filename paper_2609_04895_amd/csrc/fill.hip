@@ -25,24 +25,32 @@ namespace {
 constexpr int kFillThreads = 256;
 
 // Block-wide exclusive prefix counts and sums over the 256 threads of the
-// block, each with one barrier: the wavefront totals go to a four-entry
-// slot of LDS, and consecutive calls use different slots, so no barrier is
-// needed after one call before the next.  *total gets the block total.
-// Flags: the ballot bits below the lane.
-__device__ int block_count(bool v, int* total, int* slot) {
+// block, each call with one barrier: the wavefront totals go to LDS slots
+// (four per value), and consecutive calls use different slots, so no barrier
+// is needed after one call before the next.
+// NF flags at once: the ballot bits below the lane; total[f] gets the block
+// total of flag f.  slot: 4 NF ints.
+template <int NF>
+__device__ void block_counts(const bool (&v)[NF], int (&below)[NF], int (&total)[NF], int* slot) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const unsigned long long b = __ballot(v);
-    const int below = (int)__builtin_amdgcn_mbcnt_hi((unsigned)(b >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)b, 0u));
-    if (lane == 0) slot[w] = __popcll(b);
-    __syncthreads();
-    int off = 0, tot = 0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        if (i < w) off += slot[i];
-        tot += slot[i];
+    for (int f = 0; f < NF; ++f) {
+        const unsigned long long b = __ballot(v[f]);
+        below[f] = (int)__builtin_amdgcn_mbcnt_hi((unsigned)(b >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)b, 0u));
+        if (lane == 0) slot[4 * f + w] = __popcll(b);
     }
-    *total = tot;
-    return off + below;
+    __syncthreads();
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+        int off = 0, tot = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (i < w) off += slot[4 * f + i];
+            tot += slot[4 * f + i];
+        }
+        below[f] += off;
+        total[f] = tot;
+    }
 }
 
 // Values: an inclusive wavefront scan in DPP steps (shifts by 1, 2, 4 and 8
@@ -153,7 +161,8 @@ __device__ inline unsigned long long cache_word(const Layout& lo, int layer, int
 struct FillLds {
     unsigned long long U[4];
     int so[kMaxN], se[kMaxN], stp[kMaxN], rnd_s[kMaxN], free_list[kMaxN], enter_list[kMaxN], victim_list[kMaxN];
-    int lds4[4][4];  // block-scan slots
+    int lds4[4];       // block-scan slots
+    int lds_cnt[2][12];  // block-count slots: round plan; free slots, entries, multi-pass units
     __align__(16) int key[kMaxN];
     int by_rank[kMaxN], who[kMaxN], m_rank[kMaxN];
 };
@@ -164,7 +173,7 @@ struct FillLds {
 __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs& f, FillLds& sm, int wg, int nwg) {
     unsigned long long* U = sm.U;
     int *so = sm.so, *se = sm.se, *stp = sm.stp, *rnd_s = sm.rnd_s, *free_list = sm.free_list;
-    int *enter_list = sm.enter_list, *victim_list = sm.victim_list, (*lds4)[4] = sm.lds4;
+    int *enter_list = sm.enter_list, *victim_list = sm.victim_list, *lds4 = sm.lds4;
     const int tid = threadIdx.x;
     const int N = lo.N, layer = f.layer, P = lo.n_slots;
     const int64_t vin = (int64_t)f.rv * lo.L + layer, vout = (int64_t)(f.rv ^ 1) * lo.L + layer;
@@ -236,10 +245,10 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
             rnd = inE ? 0 : -1;
         } else if (f.round == 0) {
             const bool res_e = inE && cur >= 0, mis_e = inE && cur < 0;
-            int nres, nmis;
-            const int r1 = block_count(res_e, &nres, lds4[0]);
-            const int r2 = block_count(mis_e, &nmis, lds4[1]);
-            rnd = res_e ? r1 / P : (mis_e ? (nres + r2) / P : -1);
+            const bool fl[2] = {res_e, mis_e};
+            int rk[2], n[2];
+            block_counts<2>(fl, rk, n, sm.lds_cnt[0]);
+            rnd = res_e ? rk[0] / P : (mis_e ? (n[0] + rk[1]) / P : -1);
         } else {
             rnd = e < N ? ro_v : -1;
         }
@@ -251,10 +260,20 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
     else if (!overflow) enter = f.round == 0 && e < N && inU && cur < 0;
     else enter = now && cur < 0;
     const bool is_free = tid < P && se[tid] == -1;
-    int nfree, nenter;
-    const int rf = block_count(is_free, &nfree, lds4[2]);
+    // The work units of this round (below) need to know whether any bucket
+    // takes more than one pass, and rank the experts by their bucket sizes
+    // if one does: the flag joins the free-slot and entry counts, and the
+    // ranking keys are stored before the same barrier.
+    const int m_own = (units && now) ? m_v : 0;
+    const int ut = lo.unit_tokens;
+    const int mykey = (m_own << 8) | (255 - tid);
+    if (units) sm.key[tid] = tid < N ? mykey : -1;  // kFillThreads == kMaxN: every entry is written
+    const bool fl[3] = {is_free, enter, units && m_own > ut};
+    int rk[3], n[3];
+    block_counts<3>(fl, rk, n, sm.lds_cnt[1]);
+    const int rf = rk[0], re = rk[1], nfree = n[0], nenter = n[1];
+    const bool multi = n[2] > 0;
     if (is_free) free_list[rf] = tid;
-    const int re = block_count(enter, &nenter, lds4[3]);
     // A round that needs more than the free slots evicts the least recently
     // used experts that no remaining round needs (lower slot on ties), ranked
     // by (stamp, slot); after refinement only free slots are filled.
@@ -321,10 +340,7 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
     // slot and its token count, so that an FFN wavefront finds all three with
     // one load.  When no bucket needs a second pass, unit e is expert e (or
     // none if it has no tokens in this round).
-    const int m_own = (units && now) ? m_v : 0;
     int4* unit4 = reinterpret_cast<int4*>(lo.units);
-    const int ut = lo.unit_tokens;
-    const bool multi = __syncthreads_or(units && m_own > ut) != 0;
     if (units && !multi) {
         // kFillThreads >= N: thread e holds expert e's bucket size
         for (int i = tid; i < lo.max_units; i += kFillThreads)
@@ -333,17 +349,21 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         // otherwise experts with more tokens go first (lower index on ties),
         // so the longest units start first.  Rank of expert e = number of
         // larger keys (m << 8) | (255 - e), all distinct.
-        int *key = sm.key, *by_rank = sm.by_rank, *who = sm.who, *m_rank = sm.m_rank;
+        // (the keys were stored before the barrier of the counts above)
+        int *by_rank = sm.by_rank, *who = sm.who, *m_rank = sm.m_rank;
         const int m = m_own;
-        const int mykey = (m << 8) | (255 - tid);
-        key[tid] = tid < N ? mykey : -1;  // kFillThreads == kMaxN: every entry is written
-        __syncthreads();
         int rank = 0;
         if (tid < N) {
-            const int4* k4 = reinterpret_cast<const int4*>(key);
-            for (int u = 0; u < (N + 3) / 4; ++u) {
-                const int4 v = k4[u];
-                rank += (v.x > mykey) + (v.y > mykey) + (v.z > mykey) + (v.w > mykey);
+            // batches of 32 keys, every LDS read of a batch issued before the
+            // first compare; keys past N are -1 and never counted
+            const int4* k4 = reinterpret_cast<const int4*>(sm.key);
+            for (int u0 = 0; u0 < (N + 3) / 4; u0 += 8) {  // u0 + 7 < kMaxN / 4
+                int4 v[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) v[i] = k4[u0 + i];
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    rank += (v[i].x > mykey) + (v[i].y > mykey) + (v[i].z > mykey) + (v[i].w > mykey);
             }
         }
         if (tid < N) {
@@ -354,7 +374,7 @@ __device__ __forceinline__ void residency_event(const Layout& lo, const FillArgs
         __syncthreads();
         const int passes = tid < N ? by_rank[tid] : 0;
         int total;
-        const int off = block_scan(passes, &total, lds4[0]);
+        const int off = block_scan(passes, &total, lds4);
         if (tid < N) {
             const int e = who[tid];
             for (int q = 0; q < passes; ++q)
