@@ -205,6 +205,16 @@ def test_bf16_buckets_of_hundreds_of_tokens(shape):
     run_e2e(w, T=3, tol=2e-2, ffn_shape=shape)
 
 
+@pytest.mark.parametrize("shape", ["single", "grouped"])
+def test_bf16_multi_pass_units_with_ragged_expert_count(shape):
+    # 37 experts (not a multiple of 4 or 16) under Zipf skew, 300 streams,
+    # top-3: the hot experts' buckets take several work units, so the fill
+    # kernel ranks all 37 bucket sizes (keys past N read as padding)
+    w = synth.WORKLOADS["qwen3_30b_zipf"].replace(name="bf16_n37_multi", L=1, N=37, K=3, d=128, F=64, S=300, C=5,
+                                                  R=2)
+    run_e2e(w, T=3, tol=2e-2, ffn_shape=shape)
+
+
 def test_bf16_large_hidden_dims():
     # d = 8192, F = 4096: 201 MB per expert, 128 k chunks per gate/up tile,
     # router ranges at the largest split length
