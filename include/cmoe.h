@@ -294,8 +294,10 @@ cmoe_status cmoe_read(cmoe_handle* hd, int32_t view, void* host_out, size_t byte
  * timestamps (hipExtLaunchKernel);
  * cmoe_profile_end synchronizes and returns, per kernel id, the summed
  * milliseconds and the launch count.  Kernel ids: 0 router GEMV, 1 cache
- * step (routing, refinement, retention, counters, expert grouping),
- * 2 residency and fill, 3 expert gate/up, 4 expert down, 5 combine.
+ * step (routing, refinement, retention, counters, expert grouping; from the
+ * second layer on, the same launch also runs the previous layer's combine),
+ * 2 residency and fill, 3 expert gate/up, 4 expert down, 5 combine of the
+ * last layer (one launch per token).
  * ms_out and launches_out hold CMOE_KERNEL_COUNT entries.  Timed launches
  * carry extra bookkeeping; time few kernels at once. */
 #define CMOE_KERNEL_COUNT 6

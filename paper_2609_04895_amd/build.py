@@ -8,7 +8,7 @@ import sys
 _HERE = os.path.dirname(os.path.abspath(__file__))
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 LIB = os.path.join(_HERE, "libcmoe.so")
-SOURCES = ["router.hip", "cache.hip", "fill.hip", "ffn.hip", "probe.hip", "cmoe.cpp"]
+SOURCES = ["router.hip", "cache.hip", "fill.hip", "ffn.hip", "combine.hip", "probe.hip", "cmoe.cpp"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

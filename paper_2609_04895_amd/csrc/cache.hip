@@ -45,6 +45,7 @@
 #include <math.h>
 
 #include "cmoe_internal.h"
+#include "combine.h"
 
 namespace cmoe {
 
@@ -606,14 +607,27 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
     }
 }
 
+// grid: the stream workgroups, then (a.y non-NULL) the workgroups of the
+// previous layer's combine.  The combine's only input, the gated expert
+// outputs, is complete once the previous layer's FFN has run, and no step of
+// this launch reads its output, so it runs here on the compute units that the
+// stream wavefronts leave idle, in place of a launch of its own; its
+// workgroups come after the streams' in dispatch order, so their loads queue
+// behind the streams' prologue loads.
 template <int NPL, int NR, bool INJECT, int ZS>
 __global__ __launch_bounds__(64 * kStreamsPerBlock) void cache_step_kernel(Layout lo, StepArgs a) {
+    constexpr int kThreads = 64 * kStreamsPerBlock;
+    const int nsb = (lo.S + kStreamsPerBlock - 1) / kStreamsPerBlock;
+    if ((int)blockIdx.x >= nsb) {
+        combine_quad(lo, a.cl, a.y, (int64_t)(blockIdx.x - nsb) * kThreads + threadIdx.x);
+        return;
+    }
     const int lane = threadIdx.x & 63;
     const int s = blockIdx.x * kStreamsPerBlock + (threadIdx.x >> 6);
     if ((a.flags & kFlagAccess) && blockIdx.x == 0) {
         // the other bucket buffer was used by the previous layer step (its FFN
         // has completed) and is filled by the next one
-        for (int i = threadIdx.x; i < lo.N; i += blockDim.x) lo.bcount[(int64_t)(a.bbuf ^ 1) * lo.N + i] = 0;
+        for (int i = threadIdx.x; i < lo.N; i += kThreads) lo.bcount[(int64_t)(a.bbuf ^ 1) * lo.N + i] = 0;
     }
     if (s < lo.S) stream_step<NPL, NR, INJECT, ZS>(lo, a, s, lane);  // wave-uniform branch
 }
@@ -667,7 +681,9 @@ hipError_t launch_prep_workspace(const Layout& lo, hipStream_t st) {
 
 template <int NPL, int NR>
 hipError_t launch_step_nr(const Layout& lo, const StepArgs& a, hipStream_t st, const Timing& tm) {
-    const dim3 grid((lo.S + kStreamsPerBlock - 1) / kStreamsPerBlock);
+    const int64_t nsb = (lo.S + kStreamsPerBlock - 1) / kStreamsPerBlock;
+    const int64_t quads = a.y ? (int64_t)lo.S * (lo.d / 4) : 0;  // combine threads
+    const dim3 grid((unsigned)(nsb + (quads + 64 * kStreamsPerBlock - 1) / (64 * kStreamsPerBlock)));
     const dim3 block(64 * kStreamsPerBlock);
     if (a.flags & kFlagInject)
         launch_kernel(cache_step_kernel<NPL, NR, true, 2>, grid, block, st, tm, lo, a);

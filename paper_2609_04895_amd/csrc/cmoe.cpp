@@ -348,6 +348,10 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
         StepArgs a{l, l + 1, hd->R, bbuf, flags, hd->t, {zR, nullptr, nullptr}};
         if (hd->dv.iT > 0) a.z[hd->dv.iT] = zT;
         if (hd->dv.iS > 0) a.z[hd->dv.iS] = zS;
+        if (!inject && l > 0) {  // the same launch combines layer l - 1's expert outputs
+            a.y = y;
+            a.cl = l - 1;
+        }
         HIPCHK(timed(hd, KID_CACHE, [&](const cmoe::Timing& tm) { return cmoe::launch_cache_step(lo, a, M, tm); }),
                "cache step");
         hd->g += 1;
@@ -383,10 +387,10 @@ cmoe_status run_token(cmoe_handle* hd, const void* h, float* y, const float* zR,
                        "ffn down");
             }
         }
-        if (!inject)
-            HIPCHK(timed(hd, KID_COMBINE, [&](const cmoe::Timing& tm) { return cmoe::launch_combine(lo, l, y, M, tm); }),
-                   "combine");
     }
+    if (!inject)
+        HIPCHK(timed(hd, KID_COMBINE, [&](const cmoe::Timing& tm) { return cmoe::launch_combine(lo, c.L - 1, y, M, tm); }),
+               "combine");
     hd->t += 1;
     if (hd->prof_left > 0) hd->prof_left -= 1;
     return CMOE_OK;

@@ -89,6 +89,8 @@ struct StepArgs {
     uint32_t flags;
     int32_t t;          // token index (LRU clock)
     const float* z[3];  // injected logits [S][L][N] per router slot (kFlagInject)
+    float* y;           // non-NULL: the launch also combines layer cl's expert outputs into y
+    int32_t cl;
 };
 
 // One residency event of layer `layer` (or one round of it): the arena must

@@ -653,41 +653,6 @@ __global__ __launch_bounds__(64) void ffn_down_f32(Layout lo, int l, int bbuf, i
     }
 }
 
-// ---------------------------------------------------------------- combine
-// four wavefronts per workgroup (measured slightly faster than one)
-constexpr int kCombineThreads = 256;
-
-__global__ __launch_bounds__(kCombineThreads) void combine_kernel(Layout lo, int l, float* __restrict__ y) {
-    const int n4 = lo.d / 4;
-    const int64_t idx = (int64_t)blockIdx.x * kCombineThreads + threadIdx.x;
-    if (idx >= (int64_t)lo.S * n4) return;
-    const int s = (int)(idx / n4), c = (int)(idx - (int64_t)s * n4);
-    const float4* yp = reinterpret_cast<const float4*>(lo.yp) + (int64_t)s * lo.K * n4 + c;
-    // Batches of 8 outputs: every load of a batch (indices clamped to K - 1;
-    // a clamped re-read is not added) is issued before the adds, which run
-    // in k order.
-    const int K = lo.K;
-    float4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < K; k0 += 8) {
-        float4 v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = yp[(int64_t)min(k0 + u, K - 1) * n4];
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            if (k0 + u == 0) {
-                acc = v[0];
-            } else if (k0 + u < K) {
-                acc.x = acc.x + v[u].x;
-                acc.y = acc.y + v[u].y;
-                acc.z = acc.z + v[u].z;
-                acc.w = acc.w + v[u].w;
-            }
-        }
-    }
-    reinterpret_cast<float4*>(y + ((int64_t)s * lo.L + l) * lo.d)[c] = acc;
-}
-
 }  // namespace
 
 hipError_t launch_ffn_up(const Layout& lo, int l, int bbuf, int sv, int round, const void* h, hipStream_t st,
@@ -717,13 +682,6 @@ hipError_t launch_ffn_down(const Layout& lo, int l, int bbuf, int sv, int round,
     } else {
         launch_kernel(ffn_down_f32, dim3(lo.N * (lo.d / 64)), dim3(64), st, tm, lo, l, bbuf, sv, round);
     }
-    return hipGetLastError();
-}
-
-hipError_t launch_combine(const Layout& lo, int l, float* y, hipStream_t st, const Timing& tm) {
-    const int64_t n = (int64_t)lo.S * (lo.d / 4);
-    launch_kernel(combine_kernel, dim3((unsigned)((n + kCombineThreads - 1) / kCombineThreads)), dim3(kCombineThreads),
-                  st, tm, lo, l, y);
     return hipGetLastError();
 }
 
