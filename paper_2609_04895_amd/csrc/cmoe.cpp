@@ -74,6 +74,7 @@ struct Derived {
     int rounds;        // FFN rounds per layer step: more than one only for an arena smaller than the union
     int iT, iS;        // router slots of the Temporal / Spatio Router, -1 if not used
     int ffn_waves;     // wavefronts per bf16 FFN workgroup (1 or 4)
+    int xcd_units;     // 1: each FFN work unit's workgroups on one XCD
     size_t esz, expert_bytes;
 };
 
@@ -116,6 +117,10 @@ cmoe_status validate(const cmoe_config* c, Derived* dv) {
     dv->ffn_waves = (c->flags & CMOE_FLAG_FFN_GROUPED) ? 4
                     : (c->flags & CMOE_FLAG_FFN_SINGLE) ? 1
                     : ((int64_t)c->S * c->K >= (int64_t)8 * c->N ? 4 : 1);
+    // a work unit's workgroups on one XCD (its tokens' activations fetched
+    // into one L2) pay off from 4 tokens per expert on average; with fewer,
+    // spreading each unit over all XCDs streams the weights faster
+    dv->xcd_units = (int64_t)c->S * c->K >= (int64_t)4 * c->N ? 1 : 0;
     dv->NW = (c->N + 63) / 64;
     const bool temporal = c->policy == CMOE_POLICY_ROUTER;
     dv->iT = temporal ? 1 : -1;
@@ -516,6 +521,7 @@ cmoe_status cmoe_init(const cmoe_config* cfg, const cmoe_weights* w, const cmoe_
     lo.slot_stamp = reinterpret_cast<int32_t*>(sb + p.slot_stamp);
     lo.max_units = max_units(cfg);
     lo.ffn_waves = dv.ffn_waves;
+    lo.xcd_units = dv.xcd_units;
     lo.unit_tokens = dv.ffn_waves > 1 ? cmoe::kUnitTokensGrouped : cmoe::kUnitTokens;
     hd->lo_static = lo;
     bind_workspace(lo, static_cast<char*>(buf->workspace), p);

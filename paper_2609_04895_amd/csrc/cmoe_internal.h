@@ -32,6 +32,8 @@ struct Layout {
     int32_t unit_tokens;   // tokens per work unit: kUnitTokens, or kUnitTokensGrouped (grouped launch)
     int32_t ffn_waves;     // wavefronts per bf16 FFN workgroup: 1, or 4 (grouped: units of more
                            // than 16 tokens share their activations through LDS)
+    int32_t xcd_units;     // 1: the bf16 FFN grids put each work unit's workgroups on one XCD,
+                           // 0: on all XCDs in turn
     int32_t policy;        // retention priority (cmoe_policy)
     float lrfu_w;          // LRFU decay per token, fl32(2^-lambda)
     int64_t expert_elems;  // 3 d F

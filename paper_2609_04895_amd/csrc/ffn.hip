@@ -77,20 +77,29 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
     return (a >> 16) | (b & 0xFFFF0000u);
 }
 
-// The FFN grids hold wgn workgroups per work unit.  Workgroup b takes unit
+// The FFN grids hold wgn workgroups per work unit; consecutive workgroups go
+// to the eight XCDs in turn.  With xcd_units, workgroup b takes unit
 // u = 8 (q / wgn) + b % 8 and part q % wgn of it, q = b / 8, so that all the
-// workgroups of a unit have the same b % 8.  Consecutive workgroups go to the
-// eight XCDs in turn, so a unit runs on one XCD and its tokens' activations
-// are fetched into one L2 instead of eight.  Units come heaviest first, and
-// each XCD takes every eighth one.  The grid is rounded up to whole groups
-// of eight units; u may exceed the last unit.
-__device__ inline void unit_of_block(int b, int wgn, int& u, int& j) {
-    const int q = b >> 3, g = q / wgn;
-    u = g * 8 + (b & 7);
-    j = q - g * wgn;
+// workgroups of a unit have the same b % 8: a unit runs on one XCD and its
+// tokens' activations are fetched into one L2 instead of eight.  Units come
+// heaviest first, and each XCD takes every eighth one.  That grid is rounded
+// up to whole groups of eight units; u may exceed the last unit.  Without
+// it, workgroup b takes unit b / wgn, part b % wgn, and every unit is spread
+// over all XCDs: with few tokens per expert there is little to share, and
+// whole units per XCD were measured to stream the weights more slowly (up to
+// 15% at one token per expert).
+__device__ inline void unit_of_block(int b, int wgn, bool xcd, int& u, int& j) {
+    if (xcd) {
+        const int q = b >> 3, g = q / wgn;
+        u = g * 8 + (b & 7);
+        j = q - g * wgn;
+    } else {
+        u = b / wgn;
+        j = b - u * wgn;
+    }
 }
 
-inline int unit_groups(const Layout& lo) { return (lo.max_units + 7) / 8 * 8; }
+inline int unit_groups(const Layout& lo) { return lo.xcd_units ? (lo.max_units + 7) / 8 * 8 : lo.max_units; }
 
 __device__ inline const uint16_t* slot_base(const Layout& lo, int l, int slot) {
     return reinterpret_cast<const uint16_t*>(lo.arena) + ((int64_t)l * lo.n_slots + slot) * lo.expert_elems;
@@ -426,7 +435,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(3))) voi
                                                       const uint16_t* __restrict__ h) {
     const int wgn = lo.F / (16 * W);
     int u, j;
-    unit_of_block(blockIdx.x, wgn, u, j);
+    unit_of_block(blockIdx.x, wgn, lo.xcd_units != 0, u, j);
     if (u >= lo.max_units) return;
     const int lane = threadIdx.x & 63;
     const int ft = j * W + (threadIdx.x >> 6);
@@ -553,7 +562,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(3))) voi
     const int dtn = lo.d / 32;
     const int wgn = (dtn + W - 1) / W;
     int u, j;
-    unit_of_block(blockIdx.x, wgn, u, j);
+    unit_of_block(blockIdx.x, wgn, lo.xcd_units != 0, u, j);
     if (u >= lo.max_units) return;
     const int lane = threadIdx.x & 63;
     const int dt = j * W + (threadIdx.x >> 6);
