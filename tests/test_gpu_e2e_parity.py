@@ -215,6 +215,40 @@ def test_bf16_multi_pass_units_with_ragged_expert_count(shape):
     run_e2e(w, T=3, tol=2e-2, ffn_shape=shape)
 
 
+@pytest.mark.parametrize("base,N", [("qwen3_30b", 16), ("qwen3_30b_zipf", 64)])
+def test_bf16_combine_in_the_next_cache_step_ragged_tail(base, N):
+    # From the second layer on, the cache-step launch also combines the
+    # previous layer's gated outputs in workgroups after the streams': 37
+    # streams x d = 192 leave the last of them part-filled, K = 5 a part-filled
+    # batch of outputs.  N = 16: 11.6 tokens per expert, each FFN work unit on
+    # one XCD; N = 64 (full mode, with the refine-only launch of layer 0):
+    # 2.9, units spread over all XCDs.
+    w = synth.WORKLOADS[base].replace(name=f"bf16_combine_tail_{base}_{N}", L=3, N=N, K=5, d=192, F=128, S=37,
+                                      C=6, R=2)
+    run_e2e(w, T=3, tol=2e-2)
+
+
+def test_profile_counts_one_combine_launch_per_token():
+    from paper_2609_04895_amd.workload import engine_for
+    w = synth.WORKLOADS["qwen3_30b"].replace(name="profile_counts", L=4, N=16, K=2, d=128, F=64, S=8, C=4, R=0)
+    say(f"profile counts {w.name}")
+    inp = synth.device_inputs(w, T=3)
+    eng = engine_for(w, inp)
+    y = torch.empty((w.S, w.L, w.d), dtype=torch.float32, device=torch.device("cuda", 0))
+    eng.cmoe_step(inp["hidden"][0], y)
+    eng.cmoe_profile_begin(2)
+    for t in (1, 2):
+        eng.cmoe_step(inp["hidden"][t], y)
+    prof = eng.cmoe_profile_end()
+    per_layer = {"router": 2 * w.L, "cache_step": 2 * w.L, "fill": 2 * w.L, "ffn_up": 2 * w.L, "ffn_down": 2 * w.L,
+                 "combine": 2}
+    for k, n in per_layer.items():
+        assert prof[k][1] == n, (k, prof[k])
+        assert prof[k][0] > 0, k
+    eng.cmoe_destroy()
+    del inp
+
+
 def test_bf16_large_hidden_dims():
     # d = 8192, F = 4096: 201 MB per expert, 128 k chunks per gate/up tile,
     # router ranges at the largest split length
