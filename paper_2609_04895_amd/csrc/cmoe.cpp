@@ -200,7 +200,7 @@ Plan make_plan(const cmoe_config* c, const Derived& dv) {
     p.bcount = take(2 * N * 4);
     p.pairs = take(2 * N * S * 4);
     p.act = take(S * K * (size_t)c->F * dv.esz);
-    p.yp = take(S * K * (size_t)c->d * 4);
+    p.yp = take(S * K * (size_t)c->d * dv.esz);
     p.zero_row = take(N * 4);
     p.units = take((size_t)max_units(c) * 16);
     p.round_of = take(N * 4);
@@ -221,7 +221,7 @@ void bind_workspace(Layout& lo, char* wb, const Plan& p) {
     lo.bcount = reinterpret_cast<int32_t*>(at(p.bcount));
     lo.pairs = reinterpret_cast<int32_t*>(at(p.pairs));
     lo.act = at(p.act);
-    lo.yp = reinterpret_cast<float*>(at(p.yp));
+    lo.yp = at(p.yp);
     lo.zero_row = reinterpret_cast<float*>(at(p.zero_row));
     lo.units = reinterpret_cast<int32_t*>(at(p.units));
     lo.round_of = reinterpret_cast<int32_t*>(at(p.round_of));

@@ -67,7 +67,7 @@ struct Layout {
     int32_t* bcount;            // [2][N]      tokens per expert (two buffers)
     int32_t* pairs;             // [2][N][S]   (stream << 8) | k of each token of an expert
     void* act;                  // [S][K][F]   SwiGLU intermediate (dtype)
-    float* yp;                  // [S][K][d]   gated expert outputs
+    void* yp;                   // [S][K][d]   gated expert outputs (dtype)
     float* zero_row;            // [N]         zeros (native bias when there is none)
     int32_t* units;             // [max_units][4] FFN work units of the current round, heaviest
                                 //             first: {(pass << 8) | expert, slot, tokens, 0},

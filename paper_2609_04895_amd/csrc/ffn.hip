@@ -77,6 +77,16 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
     return (a >> 16) | (b & 0xFFFF0000u);
 }
 
+// Gated output of (stream s, slot k) at d-rows j .. j + 3 (c0) and
+// j + 16 .. j + 19 (c1), rounded to bf16 like the SwiGLU intermediate: the
+// combine adds them in fp32.
+__device__ inline void store_gated(const Layout& lo, int s, int k, int j, float gk, const f32x4& c0, const f32x4& c1) {
+    uint16_t* dst = reinterpret_cast<uint16_t*>(lo.yp) + ((int64_t)s * lo.K + k) * lo.d + j;
+    *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(gk * c0[0], gk * c0[1]), pack_bf16x2(gk * c0[2], gk * c0[3]));
+    *reinterpret_cast<uint2*>(dst + 16) =
+        make_uint2(pack_bf16x2(gk * c1[0], gk * c1[1]), pack_bf16x2(gk * c1[2], gk * c1[3]));
+}
+
 // The FFN grids hold wgn workgroups per work unit; consecutive workgroups go
 // to the eight XCDs in turn.  With xcd_units, workgroup b takes unit
 // u = 8 (q / wgn) + b % 8 and part q % wgn of it, q = b / 8, so that all the
@@ -484,10 +494,7 @@ __device__ inline void down_passes(const Layout& lo, int l, int dt, const int32_
             if (tok < m) {
                 const int s = pr[q] >> 8, k = pr[q] & 255;
                 const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
-                float* dst = lo.yp + ((int64_t)s * lo.K + k) * lo.d + dt * 32 + 4 * g;
-                *reinterpret_cast<float4*>(dst) = make_float4(gk * c0[q][0], gk * c0[q][1], gk * c0[q][2], gk * c0[q][3]);
-                *reinterpret_cast<float4*>(dst + 16) =
-                    make_float4(gk * c1[q][0], gk * c1[q][1], gk * c1[q][2], gk * c1[q][3]);
+                store_gated(lo, s, k, dt * 32 + 4 * g, gk, c0[q], c1[q]);
             }
         }
     }
@@ -517,10 +524,7 @@ __device__ inline void down_heavy(const Layout& lo, int l, int dt, bool active, 
         if (tok < m) {
             const int s = pr[q] >> 8, k = pr[q] & 255;
             const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
-            float* dst = lo.yp + ((int64_t)s * lo.K + k) * lo.d + dt * 32 + 4 * g;
-            *reinterpret_cast<float4*>(dst) = make_float4(gk * c0[q][0], gk * c0[q][1], gk * c0[q][2], gk * c0[q][3]);
-            *reinterpret_cast<float4*>(dst + 16) =
-                make_float4(gk * c1[q][0], gk * c1[q][1], gk * c1[q][2], gk * c1[q][3]);
+            store_gated(lo, s, k, dt * 32 + 4 * g, gk, c0[q], c1[q]);
         }
     }
 }
@@ -548,10 +552,7 @@ __device__ __forceinline__ void down_heavy_wide(const Layout& lo, int l, int dt,
             const int pair = bk[tok];
             const int s = pair >> 8, k = pair & 255;
             const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
-            float* dst = lo.yp + ((int64_t)s * lo.K + k) * lo.d + dt * 32 + 4 * g;
-            *reinterpret_cast<float4*>(dst) = make_float4(gk * c0[q][0], gk * c0[q][1], gk * c0[q][2], gk * c0[q][3]);
-            *reinterpret_cast<float4*>(dst + 16) =
-                make_float4(gk * c1[q][0], gk * c1[q][1], gk * c1[q][2], gk * c1[q][3]);
+            store_gated(lo, s, k, dt * 32 + 4 * g, gk, c0[q], c1[q]);
         }
     }
 }
@@ -658,7 +659,7 @@ __global__ __launch_bounds__(64) void ffn_down_f32(Layout lo, int l, int bbuf, i
             for (int u = 0; u < 32; ++u) acc = __builtin_fmaf(wd[u], a32[u], acc);
         }
         const float gk = lo.gates[((int64_t)l * lo.S + s) * lo.K + k];
-        lo.yp[((int64_t)s * lo.K + k) * lo.d + j] = gk * acc;
+        reinterpret_cast<float*>(lo.yp)[((int64_t)s * lo.K + k) * lo.d + j] = gk * acc;
     }
 }
 
