@@ -612,8 +612,8 @@ __device__ void stream_step(const Layout& lo, const StepArgs& a, int s, int lane
 // outputs, is complete once the previous layer's FFN has run, and no step of
 // this launch reads its output, so it runs here on the compute units that the
 // stream wavefronts leave idle, in place of a launch of its own; its
-// workgroups come after the streams' in dispatch order, so their loads queue
-// behind the streams' prologue loads.
+// workgroups come after the streams' in dispatch order, so the streams'
+// prologue loads are issued first.
 template <int NPL, int NR, bool INJECT, int ZS>
 __global__ __launch_bounds__(64 * kStreamsPerBlock) void cache_step_kernel(Layout lo, StepArgs a) {
     constexpr int kThreads = 64 * kStreamsPerBlock;

@@ -1,8 +1,8 @@
 // combine.h - the gated combine of one layer's expert outputs, as a device
-// function: y[s][l] = sum over k of the gated outputs yp[s][k] (the gates are
-// already applied by the down projection), added in k order in fp32.  Used by the
-// stand-alone combine kernel and by the cache-step launch of the next layer,
-// which runs it in workgroups of its own.
+// function: y[s][l] = sum over k of the gated outputs yp[s][k] (the gates
+// are already applied by the down projection), added in k order in fp32.
+// Used by the stand-alone combine kernel and by the cache-step launch of the
+// next layer, which runs it in workgroups of its own.
 #pragma once
 
 #include <type_traits>
