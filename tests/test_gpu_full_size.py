@@ -138,6 +138,13 @@ def test_full_size_qwen3_30b_update_only():
     run_full(synth.WORKLOADS["qwen3_30b"], T=24)
 
 
+@pytest.mark.parametrize("S", [16, 32])
+def test_full_size_qwen3_30b_fewer_streams(S):
+    # Fewer than 4 tokens per expert on average: the FFN grids spread every
+    # work unit over all XCDs (80-110 units per layer step at full size).
+    run_full(synth.WORKLOADS["qwen3_30b"].replace(S=S), T=12, ffn_samples=6)
+
+
 def test_full_size_gptoss_20b_full_mode():
     run_full(synth.WORKLOADS["gptoss_20b"], T=24)
 
